@@ -1,0 +1,306 @@
+/*
+ * vdref.c -- reference oracle for the ValueDiff eviction pass.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the CPU-baseline
+ * leg of the benchmark do.  It shares no source, header, table or helper with
+ * the HIP library.
+ *
+ * Everything is computed in double precision with plain loops, one unit
+ * (sequence, layer, KV head) at a time, in the order the paper states:
+ *
+ *   1. mean of the n cached value vectors, v_bar = (1/n) sum_i v_i
+ *      (Sec. 3.2, Eq. vd; the n cached tokens include the block just
+ *      appended, Sec. 2.2, Eq. block_processing);
+ *   2. a score per token (Sec. 3.2):
+ *        L2   s_j = ||v_j - v_bar||                       (Eq. vd)
+ *        Dir  s_j = 1 - cos(v_j, v_bar)                   (variant after Eq. decomp)
+ *        Norm s_j = ||v_j||                               (variant after Eq. decomp)
+ *   3. keep the N highest scores whenever n exceeds the budget N
+ *      (Sec. 2.1, Eq. eviction), ties going to the lower slot index;
+ *   4. gather K and V onto the kept set with the slot-reuse layout: the
+ *      evicted slots below N, ascending, receive the kept slots at or above N,
+ *      ascending (the layout reading of "gather" used by this project).
+ *
+ * Readings of points the paper leaves open:
+ *   - Dir when ||v_j|| * ||v_bar|| == 0: cos is taken as 0, so s_j = 1.
+ *   - Norm keeps the largest norms.
+ *   - n <= N is a no-op (eviction happens only when the cache exceeds N).
+ *
+ * Pins: every function here is checked by the CPU tests against identities
+ * and brute force that do not reuse this code (minimal-disturbance identity
+ * of Sec. 3.3 Eq. recon_error, law of cosines Eq. decomp, the Dirichlet
+ * closed form of App. A Eq. app_claim, invariances, brute-force subset
+ * search, hand-worked examples).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define VDREF_BF16 0
+#define VDREF_F32 1
+
+#define VDREF_L2 0
+#define VDREF_DIR 1
+#define VDREF_NORM 2
+
+#define VDREF_OK 0
+#define VDREF_BAD_ARG 1
+
+/* ---- element access ---------------------------------------------------- */
+
+/* A bfloat16 number is the upper half of an IEEE binary32 number. */
+static double bf16_bits_to_double(uint16_t bits)
+{
+    uint32_t w = ((uint32_t)bits) << 16;
+    float f;
+    memcpy(&f, &w, sizeof f);
+    return (double)f;
+}
+
+static double get_elem(const void *rows, int dtype, int64_t idx)
+{
+    if (dtype == VDREF_BF16)
+        return bf16_bits_to_double(((const uint16_t *)rows)[idx]);
+    return (double)((const float *)rows)[idx];
+}
+
+static size_t elem_size(int dtype) { return dtype == VDREF_BF16 ? 2 : 4; }
+
+/* Exposed for the decoding pin. */
+double vdref_decode_elem(const void *rows, int dtype, int64_t idx)
+{
+    return get_elem(rows, dtype, idx);
+}
+
+/* ---- step 1: mean (Sec. 3.2, Eq. vd) ----------------------------------- */
+
+/* v: n rows of d elements, row r starting at element r*row_stride. */
+int vdref_mean(const void *v, int dtype, int64_t n, int d, int64_t row_stride,
+               double *mean)
+{
+    if (n <= 0 || d <= 0 || !v || !mean)
+        return VDREF_BAD_ARG;
+    for (int c = 0; c < d; ++c) {
+        double sum = 0.0;
+        for (int64_t i = 0; i < n; ++i)
+            sum += get_elem(v, dtype, i * row_stride + c);
+        mean[c] = sum / (double)n;
+    }
+    return VDREF_OK;
+}
+
+/* ---- step 2: scores (Sec. 3.2) ----------------------------------------- */
+
+int vdref_score(const void *v, int dtype, int64_t n, int d, int64_t row_stride,
+                int variant, double *scores, double *mean_out)
+{
+    if (n <= 0 || d <= 0 || !v || !scores)
+        return VDREF_BAD_ARG;
+    if (variant != VDREF_L2 && variant != VDREF_DIR && variant != VDREF_NORM)
+        return VDREF_BAD_ARG;
+
+    double *mean = (double *)malloc(sizeof(double) * (size_t)d);
+    if (!mean)
+        return VDREF_BAD_ARG;
+    vdref_mean(v, dtype, n, d, row_stride, mean);
+
+    double mean_norm2 = 0.0;
+    for (int c = 0; c < d; ++c)
+        mean_norm2 += mean[c] * mean[c];
+    double mean_norm = sqrt(mean_norm2);
+
+    for (int64_t j = 0; j < n; ++j) {
+        if (variant == VDREF_L2) {
+            /* s_j = || v_j - v_bar || */
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) {
+                double diff = get_elem(v, dtype, j * row_stride + c) - mean[c];
+                acc += diff * diff;
+            }
+            scores[j] = sqrt(acc);
+        } else if (variant == VDREF_NORM) {
+            /* s_j = || v_j || */
+            double acc = 0.0;
+            for (int c = 0; c < d; ++c) {
+                double x = get_elem(v, dtype, j * row_stride + c);
+                acc += x * x;
+            }
+            scores[j] = sqrt(acc);
+        } else {
+            /* s_j = 1 - cos(v_j, v_bar), cos := 0 when either norm is zero */
+            double dot = 0.0, vn2 = 0.0;
+            for (int c = 0; c < d; ++c) {
+                double x = get_elem(v, dtype, j * row_stride + c);
+                dot += x * mean[c];
+                vn2 += x * x;
+            }
+            double denom = sqrt(vn2) * mean_norm;
+            double cosv = denom > 0.0 ? dot / denom : 0.0;
+            scores[j] = 1.0 - cosv;
+        }
+    }
+    if (mean_out)
+        memcpy(mean_out, mean, sizeof(double) * (size_t)d);
+    free(mean);
+    return VDREF_OK;
+}
+
+/* ---- step 3: top-N (Sec. 2.1, Eq. eviction) ---------------------------- */
+
+typedef struct {
+    double s;
+    int64_t j;
+} scored_index;
+
+/* Higher score first; equal scores: lower index first. */
+static int by_score_desc_index_asc(const void *pa, const void *pb)
+{
+    const scored_index *a = (const scored_index *)pa;
+    const scored_index *b = (const scored_index *)pb;
+    if (a->s > b->s)
+        return -1;
+    if (a->s < b->s)
+        return 1;
+    if (a->j < b->j)
+        return -1;
+    if (a->j > b->j)
+        return 1;
+    return 0;
+}
+
+/* keep[j] = 1 for the N kept slots, 0 otherwise, for j < n. */
+int vdref_select_topn(const double *scores, int64_t n, int64_t N, uint8_t *keep)
+{
+    if (n < 0 || N < 1 || !keep || (n > 0 && !scores))
+        return VDREF_BAD_ARG;
+    if (n <= N) {
+        for (int64_t j = 0; j < n; ++j)
+            keep[j] = 1;
+        return VDREF_OK;
+    }
+    scored_index *order = (scored_index *)malloc(sizeof(scored_index) * (size_t)n);
+    if (!order)
+        return VDREF_BAD_ARG;
+    for (int64_t j = 0; j < n; ++j) {
+        order[j].s = scores[j];
+        order[j].j = j;
+    }
+    qsort(order, (size_t)n, sizeof(scored_index), by_score_desc_index_asc);
+    for (int64_t j = 0; j < n; ++j)
+        keep[j] = 0;
+    for (int64_t r = 0; r < N; ++r)
+        keep[order[r].j] = 1;
+    free(order);
+    return VDREF_OK;
+}
+
+/* ---- step 4: gather with slot reuse ------------------------------------ */
+
+static void copy_row(void *base, int dtype, int64_t row_stride, int d,
+                     int64_t dst, int64_t src)
+{
+    size_t es = elem_size(dtype);
+    char *b = (char *)base;
+    memmove(b + (size_t)(dst * row_stride) * es, b + (size_t)(src * row_stride) * es,
+            (size_t)d * es);
+}
+
+/*
+ * holes  = evicted slots in [0, N), ascending
+ * movers = kept slots in [N, n), ascending
+ * the k-th mover's K row, V row and pos entry are copied onto the k-th hole.
+ * Afterwards the kept tokens occupy slots [0, N).
+ */
+int vdref_compact(void *k, void *v, int dtype, int64_t n, int64_t N, int d,
+                  int64_t row_stride, const uint8_t *keep, int32_t *pos)
+{
+    if (n < 0 || N < 1 || d <= 0 || !keep)
+        return VDREF_BAD_ARG;
+    if (n <= N)
+        return VDREF_OK;
+    int64_t next_mover = N;
+    for (int64_t hole = 0; hole < N; ++hole) {
+        if (keep[hole])
+            continue;
+        while (next_mover < n && !keep[next_mover])
+            ++next_mover;
+        if (next_mover >= n)
+            break;
+        if (k)
+            copy_row(k, dtype, row_stride, d, hole, next_mover);
+        if (v)
+            copy_row(v, dtype, row_stride, d, hole, next_mover);
+        if (pos)
+            pos[hole] = pos[next_mover];
+        ++next_mover;
+    }
+    return VDREF_OK;
+}
+
+/* ---- the whole pass over a batch of units ------------------------------ */
+
+/*
+ * k, v       : [U][cap][d] contiguous, in place (either may be NULL)
+ * n_unit[u]  : cached tokens of unit u before eviction (0 <= n <= cap)
+ * N_unit[u]  : budget of unit u (>= 1)
+ * scores     : optional [U][cap] output (first n of each unit written)
+ * keep       : optional [U][cap] output (first n of each unit written)
+ * mean_out   : optional [U][d] output (units with n > 0)
+ * pos        : optional [U][cap] payload moved with the rows
+ * nthreads   : OpenMP threads over units (<= 0: library default)
+ */
+int vdref_evict_step(void *k, void *v, int dtype, int64_t U, int64_t cap, int d,
+                     const int32_t *n_unit, const int32_t *N_unit, int variant,
+                     double *scores, uint8_t *keep, double *mean_out,
+                     int32_t *pos, int nthreads)
+{
+    if (U < 0 || cap < 0 || d <= 0 || !v || !n_unit || !N_unit)
+        return VDREF_BAD_ARG;
+    if (dtype != VDREF_BF16 && dtype != VDREF_F32)
+        return VDREF_BAD_ARG;
+    if (variant != VDREF_L2 && variant != VDREF_DIR && variant != VDREF_NORM)
+        return VDREF_BAD_ARG;
+    for (int64_t u = 0; u < U; ++u)
+        if (n_unit[u] < 0 || n_unit[u] > cap || N_unit[u] < 1)
+            return VDREF_BAD_ARG;
+
+    size_t es = elem_size(dtype);
+    int status = VDREF_OK;
+#ifdef _OPENMP
+    if (nthreads <= 0)
+        nthreads = omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 1) num_threads(nthreads)
+#endif
+    for (int64_t u = 0; u < U; ++u) {
+        int64_t n = n_unit[u], N = N_unit[u];
+        if (n == 0)
+            continue;
+        char *vu = (char *)v + (size_t)(u * cap * d) * es;
+        char *ku = k ? (char *)k + (size_t)(u * cap * d) * es : NULL;
+        int32_t *pu = pos ? pos + u * cap : NULL;
+        double *su = (double *)malloc(sizeof(double) * (size_t)n);
+        uint8_t *keepu = (uint8_t *)malloc((size_t)n);
+        if (!su || !keepu) {
+            free(su);
+            free(keepu);
+            status = VDREF_BAD_ARG;
+            continue;
+        }
+        vdref_score(vu, dtype, n, d, d, variant, su,
+                    mean_out ? mean_out + u * d : NULL);
+        vdref_select_topn(su, n, N, keepu);
+        vdref_compact(ku, vu, dtype, n, N, d, d, keepu, pu);
+        if (scores)
+            memcpy(scores + u * cap, su, sizeof(double) * (size_t)n);
+        if (keep)
+            memcpy(keep + u * cap, keepu, (size_t)n);
+        free(su);
+        free(keepu);
+    }
+    return status;
+}

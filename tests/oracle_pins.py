@@ -1,0 +1,360 @@
+"""Pins of the C oracle: checks against what the paper and the mathematics fix.
+
+None of these checks reuses the oracle's own arithmetic.  Each check takes an
+``oracle.Oracle`` so that the same checks also run against deliberately
+mutated builds of ``oracle/vdref.c`` (see ``test_oracle_mutants.py``): every
+plausible mistake planted there must fail at least one check here.
+
+Pins and what they fix:
+  worked examples     hand-derived exact values, Sec. 3.2 Eq. vd / Sec. 2.1 Eq. eviction
+  min. disturbance    (n-1)^2 ||o* - o*_{\\j}||^2 = s_j^2, Sec. 3.3 Eq. recon_error
+  law of cosines      links L2, Dir and Norm, Sec. 3.2 Eq. decomp
+  Dirichlet           Monte Carlo of App. A Eq. app_claim (closed form with C(n))
+  invariances         translation (L2), scale, permutation (Sec. 3.3, symmetric point)
+  selection           stable sort, brute force over subsets, n = N + 1, n <= N
+  compaction          row multiset / pairing / slot-reuse layout properties
+  decoding            bf16 and fp32 element values against torch's conversion
+"""
+import itertools
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden",
+                      "worked_examples.json")
+
+
+# ---------------------------------------------------------------- helpers
+
+def _f32(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float32))
+
+
+def _rel_close(a, b, rtol, atol=0.0):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return np.all(np.abs(a - b) <= rtol * np.abs(b) + atol)
+
+
+def _frac(s: str) -> float:
+    if "sqrt2" in s:  # only the form "1-1/sqrt2" appears
+        assert s == "1-1/sqrt2"
+        return 1.0 - 1.0 / np.sqrt(2.0)
+    return float(Fraction(s))
+
+
+def _kept_list(keep):
+    return sorted(int(j) for j in np.flatnonzero(np.asarray(keep)))
+
+
+def check_decode(orc):
+    """bf16 / fp32 elements decode to the values torch's own conversion gives."""
+    import torch
+    rng = np.random.default_rng(11)
+    bits = rng.integers(0, 1 << 16, size=4096, dtype=np.uint32).astype(np.uint16)
+    bits = bits[(bits & 0x7F80) != 0x7F80]  # finite values only
+    bits = np.concatenate([bits, np.array([0x3F80, 0xC000, 0x0001, 0x8000, 0x7F7F],
+                                          dtype=np.uint16)])
+    got = orc.decode_elems(bits)
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).double().numpy()
+    assert np.array_equal(got, ref), "bf16 decoding differs from torch"
+    assert got[-5] == 1.0 and got[-4] == -2.0
+    f = rng.standard_normal(257).astype(np.float32)
+    assert np.array_equal(orc.decode_elems(f), f.astype(np.float64))
+
+
+def check_mean_library(orc):
+    """The mean is numpy's mean of the decoded rows (a library routine)."""
+    rng = np.random.default_rng(12)
+    for n, d in ((1, 3), (7, 5), (300, 64)):
+        v = _f32(rng.standard_normal((n, d)) * 3.0)
+        assert _rel_close(orc.mean(v), v.astype(np.float64).mean(axis=0), 1e-12, 1e-14)
+        b = (v.view(np.uint32) >> 16).astype(np.uint16)
+        vb = (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+        assert _rel_close(orc.mean(b), vb.mean(axis=0), 1e-12, 1e-14)
+
+
+def check_worked_examples(orc):
+    """Hand-worked examples W1-W5 (exact values derived from the definitions)."""
+    with open(GOLDEN) as fh:
+        ex = json.load(fh)["examples"]
+    for e in ex:
+        v = _f32(e["v"])
+        n = v.shape[0]
+        s, m = orc.score(v, "l2")
+        assert _rel_close(m, [_frac(x) for x in e["mean"]], 1e-15, 1e-15), e["name"]
+        assert _rel_close(s ** 2, [_frac(x) for x in e["l2_sq"]], 1e-13, 1e-15), e["name"]
+        if "norm_sq" in e:
+            sn, _ = orc.score(v, "norm")
+            assert _rel_close(sn ** 2, [_frac(x) for x in e["norm_sq"]], 1e-13, 1e-15)
+        if "dir_one_minus_cos" in e:
+            sd, _ = orc.score(v, "dir")
+            assert _rel_close(sd, [_frac(x) for x in e["dir_one_minus_cos"]], 1e-12, 1e-12)
+        ties = e.get("exact_tie", {})
+        for variant, by_n in e["kept"].items():
+            sv, _ = orc.score(v, variant)
+            for N_s, want in by_n.items():
+                got = _kept_list(orc.select_topn(sv, int(N_s)))
+                tie = ties.get(variant, {}).get(N_s)
+                if tie is None:
+                    assert got == want, (e["name"], variant, N_s, got, want)
+                else:  # exact tie at 0 in exact arithmetic: fp64 may order it either way
+                    common = sorted(set(want) - set(tie))
+                    assert set(common) <= set(got) and len(got) == len(want), (e["name"], got)
+                    assert len(set(got) & set(tie)) == len(set(want) & set(tie))
+        if "uniform_disturbance_times_n_minus_1_sq" in e:
+            assert _rel_close(s ** 2, [_frac(x) for x in
+                                       e["uniform_disturbance_times_n_minus_1_sq"]], 1e-13)
+        if "post_v" in e:
+            N = e["N"]
+            k = _f32(np.stack([np.arange(n), -np.arange(n)], axis=1))
+            vv = v.copy()
+            pos = np.arange(n, dtype=np.int32)
+            kk, vv2, pp = k[None].copy(), vv[None].copy(), pos[None].copy()
+            _, keep, _ = orc.evict_step(kk, vv2, [n], [N], "l2", pos=pp)
+            assert np.array_equal(vv2[0, :N], _f32(e["post_v"])), e["name"]
+            assert pp[0, :N].tolist() == e["post_pos"], e["name"]
+            assert kk[0, :N, 0].tolist() == e["post_pos"], e["name"]
+            assert _kept_list(keep[0, :n]) == e["kept"]["l2"][str(N)]
+
+
+def check_minimal_disturbance(orc):
+    """Sec. 3.3, Eqs. uniform_outputs / recon_error by brute force: evict each
+    token in turn, take the uniform-attention output (the mean) before and after,
+    and compare (n-1)^2 ||o* - o*_{\\j}||^2 with s_j^2; the argmin is the
+    ValueDiff argmin (Prop. vdiff_optimum)."""
+    rng = np.random.default_rng(13)
+    for trial in range(40):
+        n = int(rng.integers(2, 14))
+        d = int(rng.integers(1, 6))
+        v = _f32(rng.standard_normal((n, d)) * rng.uniform(0.1, 10.0) + rng.normal(0, 3, d))
+        x = v.astype(np.float64)
+        s, _ = orc.score(v, "l2")
+        o_all = x.sum(axis=0) / n
+        dist = np.empty(n)
+        for j in range(n):
+            rest = np.delete(x, j, axis=0)
+            o_j = rest.sum(axis=0) / (n - 1)
+            dist[j] = ((o_all - o_j) ** 2).sum() * (n - 1) ** 2
+        assert _rel_close(s ** 2, dist, 1e-9, 1e-12 * dist.max()), trial
+        if np.sort(dist)[1] > np.sort(dist)[0] * (1 + 1e-6):
+            assert int(np.argmin(s)) == int(np.argmin(dist))
+
+
+def check_law_of_cosines(orc):
+    """Sec. 3.2 Eq. decomp: s_L2^2 = s_Norm^2 - 2 s_Norm ||v_bar|| (1 - s_Dir) + ||v_bar||^2."""
+    rng = np.random.default_rng(14)
+    for trial in range(30):
+        n = int(rng.integers(2, 40))
+        d = int(rng.choice([1, 2, 3, 8, 64]))
+        v = _f32(rng.standard_normal((n, d)) + rng.normal(0, 2, d))
+        if trial % 5 == 0:
+            v[0] = 0.0  # exercises the zero-norm convention for Dir
+        s2, m = orc.score(v, "l2")
+        sd, _ = orc.score(v, "dir")
+        sn, _ = orc.score(v, "norm")
+        mn = np.sqrt((m ** 2).sum())
+        rhs = sn ** 2 - 2.0 * sn * mn * (1.0 - sd) + mn ** 2
+        scale = (sn ** 2 + mn ** 2).max()
+        assert np.all(np.abs(s2 ** 2 - rhs) <= 1e-11 * scale), trial
+
+
+def check_dirichlet(orc):
+    """App. A Eq. app_claim by Monte Carlo: with alpha ~ Dirichlet(1,...,1),
+    E[(a_j/(1-a_j))^2 ||v_j - o(a)||^2] = 2/(n(n-1)) s_j^2 + C(n),
+    C(n) = 2 (S_2 - n ||v_bar||^2) / (n^2 (n-1)(n+1))."""
+    rng = np.random.default_rng(15)
+    n, d, M = 6, 3, 400_000
+    v = _f32(rng.standard_normal((n, d)) * 2.0 + 1.0)
+    x = v.astype(np.float64)
+    s, m = orc.score(v, "l2")
+    S2 = (x ** 2).sum()
+    C = 2.0 * (S2 - n * (m ** 2).sum()) / (n ** 2 * (n - 1) * (n + 1))
+    want = 2.0 / (n * (n - 1)) * s ** 2 + C
+    alpha = rng.dirichlet(np.ones(n), size=M)          # [M, n]
+    o = alpha @ x                                       # [M, d]
+    for j in range(n):
+        w = (alpha[:, j] / (1.0 - alpha[:, j])) ** 2
+        g = w * ((x[j] - o) ** 2).sum(axis=1)
+        se = g.std() / np.sqrt(M)
+        assert abs(g.mean() - want[j]) < 6.0 * se + 1e-12, (j, g.mean(), want[j], se)
+
+
+def check_invariances(orc):
+    """Translation invariance of L2 scores, scale behaviour of all three
+    variants, permutation equivariance (integer-valued fp32 data: exact)."""
+    rng = np.random.default_rng(16)
+    for trial in range(20):
+        n = int(rng.integers(2, 30))
+        d = int(rng.integers(1, 9))
+        v = _f32(rng.integers(-8, 9, size=(n, d)))
+        c = _f32(rng.integers(-50, 51, size=d))
+        s, _ = orc.score(v, "l2")
+        st, _ = orc.score(_f32(v + c), "l2")
+        assert _rel_close(st, s, 1e-12, 1e-12), trial
+        for a in (2.0, -3.0):
+            for var, f in (("l2", abs(a)), ("norm", abs(a)), ("dir", 1.0)):
+                s0, _ = orc.score(v, var)
+                s1, _ = orc.score(_f32(v * a), var)
+                assert _rel_close(s1, f * s0, 1e-12, 1e-12), (trial, var, a)
+        perm = rng.permutation(n)
+        for var in ("l2", "dir", "norm"):
+            s0, _ = orc.score(v, var)
+            s1, _ = orc.score(_f32(v[perm]), var)
+            assert _rel_close(s1, s0[perm], 1e-12, 1e-12), (trial, var)
+
+
+def check_select_vs_sort(orc):
+    """Top-N equals the first N of a stable sort by descending score (Python's
+    sorted is stable, so equal scores keep ascending slot order)."""
+    rng = np.random.default_rng(17)
+    for trial in range(60):
+        n = int(rng.integers(1, 200))
+        N = int(rng.integers(1, n + 3))
+        s = rng.integers(0, 6, size=n).astype(np.float64) if trial % 2 else rng.random(n)
+        order = sorted(range(n), key=lambda j: -s[j])
+        want = sorted(order[:min(N, n)])
+        assert _kept_list(orc.select_topn(s, N)) == want, trial
+
+
+def check_select_bruteforce(orc):
+    """For n <= 9: the kept set is the N-subset of largest score sum, and among
+    those the one whose sorted slot list is lexicographically smallest."""
+    rng = np.random.default_rng(18)
+    for trial in range(40):
+        n = int(rng.integers(2, 10))
+        s = rng.integers(0, 4, size=n).astype(np.float64)
+        for N in range(1, n):
+            best = None
+            for sub in itertools.combinations(range(n), N):
+                key = (-sum(s[list(sub)]), list(sub))
+                if best is None or key < best:
+                    best = key
+            assert _kept_list(orc.select_topn(s, N)) == best[1], (trial, N)
+
+
+def check_select_special(orc):
+    """n = N + 1 evicts the argmin, the highest slot among equal minima;
+    n <= N keeps everything; all-equal scores keep slots [0, N)."""
+    rng = np.random.default_rng(19)
+    for trial in range(30):
+        n = int(rng.integers(2, 50))
+        s = rng.integers(0, 3, size=n).astype(np.float64)
+        keep = orc.select_topn(s, n - 1)
+        evicted = [j for j in range(n) if not keep[j]]
+        mins = [j for j in range(n) if s[j] == s.min()]
+        assert evicted == [max(mins)], trial
+        assert orc.select_topn(s, n).all() and orc.select_topn(s, n + 5).all()
+        eq = orc.select_topn(np.full(n, 2.5), n // 2 + 1)
+        assert _kept_list(eq) == list(range(n // 2 + 1))
+    v = _f32(np.tile([1.0, -2.0, 0.5], (9, 1)))
+    for var in ("l2", "dir", "norm"):
+        s, _ = orc.score(v, var)
+        assert _kept_list(orc.select_topn(s, 4)) == [0, 1, 2, 3], var
+
+
+def _check_layout(pre_ids, post_ids, keep, n, N):
+    """Slot-reuse layout properties for one unit; ids identify original slots."""
+    kept = [j for j in range(n) if keep[j]]
+    if n <= N:
+        assert list(post_ids[:n]) == list(pre_ids[:n])
+        return
+    assert len(kept) == N
+    assert sorted(post_ids[:N]) == sorted(pre_ids[j] for j in kept)
+    holes = [j for j in range(N) if not keep[j]]
+    movers = [j for j in range(N, n) if keep[j]]
+    assert len(holes) == len(movers)
+    for j in range(N):
+        if keep[j]:
+            assert post_ids[j] == pre_ids[j]  # surviving old slots stay put
+    for h, m in zip(holes, movers):
+        assert post_ids[h] == pre_ids[m]
+
+
+def check_compact(orc):
+    """Compaction invariants on random masks; K, V and pos stay paired."""
+    rng = np.random.default_rng(20)
+    for trial in range(50):
+        n = int(rng.integers(1, 80))
+        N = int(rng.integers(1, n + 3))
+        d = int(rng.integers(1, 5))
+        keep = np.zeros(n, np.uint8)
+        keep[rng.permutation(n)[:min(N, n)]] = 1
+        ids = np.arange(n)
+        k = _f32(np.repeat(ids[:, None], d, axis=1) * 2.0)
+        v = _f32(np.repeat(ids[:, None], d, axis=1) * -1.0)
+        pos = (ids + 1000).astype(np.int32)
+        orc.compact(k, v, n, N, keep, pos)
+        _check_layout(ids, (k[:, 0] / 2).astype(int), keep, n, N)
+        _check_layout(ids, (-v[:, 0]).astype(int), keep, n, N)
+        _check_layout(ids, pos - 1000, keep, n, N)
+        assert np.all(k[:, :1] == k) and np.all(v[:, :1] == v)
+
+
+def check_evict_step_batch(orc):
+    """The batched pass: per-unit n and N, ragged units, both dtypes; kept sets
+    follow the scores, the layout follows the slot-reuse rule, units stay apart."""
+    rng = np.random.default_rng(21)
+    for dt in ("f32", "bf16"):
+        U, cap, d = 7, 40, 6
+        x = rng.standard_normal((U, cap, d)).astype(np.float32)
+        v = x if dt == "f32" else (x.view(np.uint32) >> 16).astype(np.uint16)
+        v = np.ascontiguousarray(v)
+        n_unit = rng.integers(0, cap + 1, size=U).astype(np.int32)
+        n_unit[0], n_unit[1] = cap, 1
+        N_unit = rng.integers(1, cap, size=U).astype(np.int32)
+        ids = np.broadcast_to(np.arange(cap, dtype=np.int32), (U, cap)).copy()
+        k = np.ascontiguousarray(np.broadcast_to(ids[:, :, None], (U, cap, d))
+                                 .astype(np.float32))
+        if dt == "bf16":
+            k = (k.view(np.uint32) >> 16).astype(np.uint16)  # small ints are exact
+        v_pre = v.copy()
+        pos = ids.copy()
+        scores, keep, means = orc.evict_step(k, v, n_unit, N_unit, "l2", pos=pos)
+        for u in range(U):
+            n, N = int(n_unit[u]), int(N_unit[u])
+            if n == 0:
+                continue
+            s_u, m_u = orc.score(v_pre[u, :n], "l2")
+            assert np.array_equal(scores[u, :n], s_u)
+            assert np.array_equal(means[u], m_u)
+            assert np.array_equal(keep[u, :n], orc.select_topn(s_u, N))
+            _check_layout(np.arange(cap), pos[u], keep[u], n, N)
+            kd = orc.decode_elems(k[u, :, 0]).astype(int)
+            assert np.array_equal(kd, pos[u])
+            for slot in range(min(n, N)):
+                assert np.array_equal(v[u, slot], v_pre[u, pos[u, slot]])
+            assert np.array_equal(v[u, n:], v_pre[u, n:])  # beyond n: untouched
+
+
+ALL_CHECKS = [
+    check_decode, check_mean_library, check_worked_examples,
+    check_minimal_disturbance, check_law_of_cosines, check_dirichlet,
+    check_invariances, check_select_vs_sort, check_select_bruteforce,
+    check_select_special, check_compact, check_evict_step_batch,
+]
+
+
+def run_all(lib_path: str, fail_fast: bool = False) -> int:
+    """Runs every check against one build; returns the number that failed."""
+    import sys
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    from oracle.vdref import Oracle
+    orc = Oracle(lib_path)
+    failed = 0
+    for chk in ALL_CHECKS:
+        try:
+            chk(orc)
+        except Exception as exc:  # noqa: BLE001 -- any failure counts
+            failed += 1
+            print(f"FAIL {chk.__name__}: {type(exc).__name__}: {str(exc)[:200]}")
+            if fail_fast:
+                break
+    return failed
+
+
+if __name__ == "__main__":
+    import sys
+    raise SystemExit(min(run_all(sys.argv[1], fail_fast="--fail-fast" in sys.argv), 100))
