@@ -1,0 +1,274 @@
+"""Benchmark of the ValueDiff eviction pass on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one eviction pass (one ``vd_evict_step`` launch: mean, score, top-N,
+gather for every unit) over one boundary of the workload, with its inputs
+resident in HBM when timing starts.  The default workload is the
+Llama-3-8B-shaped prefill eviction (1 sequence, 32 layers x 8 KV heads,
+head_dim 128, bf16, budget 2048, block 512, prompt 32768: 60 evicting passes
+at n = 2560).  Its pre-pass states are taken from the real block-processing
+trajectory (untimed) and each timed pass consumes a fresh copy, so no pass
+sees a cache the previous one already compacted.
+
+Printed: ONE JSON line with passes/s (value), KV GB/s scanned, the roofline
+of the pass kernel (algorithmic bytes per launch / mean launch time, against
+8 TB/s) and the oracle's CPU throughput on a bounded sample.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2609_23314_amd import synth, vd  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "eviction passes/s + KV GB/s scanned (fraction of HBM peak), 1 MI355X"
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_23314_amd", "csrc", "vd_kernels.hip")
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for f in (KERNEL_SRC, os.path.join(ROOT, "paper_2609_23314_amd", "csrc", "vd_api.cpp")):
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------- trajectories
+
+def prefill_states(w: synth.Workload, count: int, dev):
+    """Pre-pass states (k, v, running_sum, n, movers per unit) of the first
+    `count` evicting boundaries of sequence-synchronous block processing."""
+    S, L, H, D, B = w.num_seqs, w.num_layers, w.num_kv_heads, w.head_dim, w.block
+    C, U = w.capacity, w.units
+    k, v = synth.empty_cache(w, dev)
+    rs = torch.zeros((U, D + 1), dtype=torch.float64, device=dev)
+    n = [0] * S
+    states = []
+    blk = 0
+    while len(states) < count:
+        for s in range(S):
+            t0 = blk * B
+            t1 = min(t0 + B, w.prompt[s])
+            if t1 > t0:
+                k[s, :, :, n[s]:n[s] + t1 - t0] = synth.block_rows(w, "k", s, blk, t0, t1, dev)
+                v[s, :, :, n[s]:n[s] + t1 - t0] = synth.block_rows(w, "v", s, blk, t0, t1, dev)
+                n[s] += t1 - t0
+        blk += 1
+        if blk * B >= max(w.prompt) and not any(a > b for a, b in zip(n, w.budget)):
+            break
+        if any(a > b for a, b in zip(n, w.budget)):
+            keep = torch.zeros((U, C), dtype=torch.uint8, device=dev)
+            snap = (k.clone(), v.clone(), rs.clone(), list(n))
+            vd.vd_evict_step(k, v, n, w.budget, "l2", running_sum=rs, keep_out=keep)
+            movers = []
+            for s in range(S):
+                N = w.budget[s]
+                us = slice(s * L * H, (s + 1) * L * H)
+                movers.append(int(keep[us, N:n[s]].sum().item()) if n[s] > N else 0)
+            states.append(snap + (movers,))
+            n = [min(a, b) for a, b in zip(n, w.budget)]
+    return states
+
+
+def algorithmic_bytes(w: synth.Workload, n, movers) -> int:
+    """One read of every cached value row, K read + K write + V write per moved
+    row, the running-sum state read and written; summed over units."""
+    L, H, D = w.num_layers, w.num_kv_heads, w.head_dim
+    row = w.row_bytes
+    total = 0
+    for s in range(w.num_seqs):
+        if n[s] > w.budget[s]:
+            total += L * H * n[s] * row + movers[s] * 3 * row
+        total += L * H * 2 * (D + 1) * 8
+    return total
+
+
+def scanned_bytes(w, n) -> int:
+    return sum(w.num_layers * w.num_kv_heads * n[s] * w.row_bytes
+               for s in range(w.num_seqs) if n[s] > w.budget[s])
+
+
+# ---------------------------------------------------------------- timing
+
+def time_pool(w, states, steps, warmup, dev):
+    """Times `steps` passes, each on a fresh copy of a pre-pass state.  Returns
+    (total seconds of the timed passes, per-launch ms, per-launch algorithmic
+    and scanned bytes)."""
+    pool_n = min(len(states), max(steps, 1))
+    work = [(st[0].clone(), st[1].clone(), st[2].clone()) for st in states[:pool_n]]
+
+    def refill(i0, cnt):
+        for j in range(cnt):
+            st = states[(i0 + j) % len(states)]
+            wk, wv, wr = work[j]
+            wk.copy_(st[0])
+            wv.copy_(st[1])
+            wr.copy_(st[2])
+
+    stream = torch.cuda.current_stream(dev)
+    done = 0
+    for i in range(warmup):
+        refill(i, 1)
+        st = states[i % len(states)]
+        vd.vd_evict_step(work[0][0], work[0][1], st[3], w.budget, "l2", running_sum=work[0][2])
+    torch.cuda.synchronize()
+    total_s, per_launch, alg, scan = 0.0, [], [], []
+    while done < steps:
+        seg = min(pool_n, steps - done)
+        refill(done, seg)
+        torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(seg + 1)]
+        t0 = time.perf_counter()
+        ev[0].record(stream)
+        for j in range(seg):
+            st = states[(done + j) % len(states)]
+            vd.vd_evict_step(work[j][0], work[j][1], st[3], w.budget, "l2",
+                             running_sum=work[j][2])
+            ev[j + 1].record(stream)
+        torch.cuda.synchronize()
+        total_s += time.perf_counter() - t0
+        for j in range(seg):
+            st = states[(done + j) % len(states)]
+            per_launch.append(ev[j].elapsed_time(ev[j + 1]))
+            alg.append(algorithmic_bytes(w, st[3], st[4]))
+            scan.append(scanned_bytes(w, st[3]))
+        done += seg
+    return total_s, per_launch, alg, scan
+
+
+# ---------------------------------------------------------------- oracle baseline
+
+def cpu_baseline(w, state, budget_s=10.0):
+    """The oracle on the host cores: whole passes over one pre-pass state."""
+    import oracle
+    k, v, _, n, _ = state
+    S, L, H, C, D = k.shape
+    kn = to_np(k).reshape(S * L * H, C, D)
+    vn = to_np(v).reshape(S * L * H, C, D)
+    nu = np.repeat(np.asarray(n, np.int32), L * H)
+    Nu = np.repeat(np.asarray(w.budget, np.int32), L * H)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    orc = oracle.load()
+    elapsed, reps = 0.0, 0
+    while elapsed < budget_s or reps == 0:
+        kc, vc = kn.copy(), vn.copy()
+        t0 = time.perf_counter()
+        orc.evict_step(kc, vc, nu, Nu, "l2", nthreads=threads)
+        elapsed += time.perf_counter() - t0
+        reps += 1
+    return {"value": reps / elapsed, "unit": "passes/s", "cores": threads, "kind": "oracle",
+            "sample": f"{reps} whole passes of one {w.name} boundary ({w.units} units, "
+                      f"n={max(n)}) in {elapsed:.1f} s",
+            "gbps_scanned": reps * scanned_bytes(w, n) / elapsed / 1e9}
+
+
+def to_np(t):
+    t = t.detach().contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def load_traffic(workload: str):
+    """HBM traffic per launch measured with rocprofv3 counters for this kernel
+    source, or None when absent or taken on another kernel version."""
+    path = os.path.join(TRAFFIC_DIR, f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        t = json.load(fh)
+    if t.get("kernel_hash") != kernel_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+# ---------------------------------------------------------------- main
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=60)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama3_8b_prefill",
+                    choices=["llama3_8b_prefill", "wide_head_d256"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the eviction pass has no cross-GPU step "
+              "(units shard across GPUs with no exchange); run it with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    vd.load()
+    w = synth.WORKLOADS[args.workload]()
+    pool = 60 if w.name == "llama3_8b_prefill" else 8
+    log(f"bench: building {pool} pre-pass states of {w.name} ...")
+    t0 = time.perf_counter()
+    states = prefill_states(w, min(pool, max(args.steps, 1)), dev)
+    log(f"bench: states ready in {time.perf_counter() - t0:.1f} s; timing {args.steps} passes")
+    total_s, per_launch, alg, scan = time_pool(w, states, args.steps, args.warmup, dev)
+    ms_launch = float(np.mean(per_launch))
+    passes_per_s = args.steps / total_s
+    kernel_s = sum(per_launch) / 1e3
+    alg_gbps = sum(alg) / kernel_s / 1e9
+    scan_gbps = sum(scan) / kernel_s / 1e9
+    log(f"bench: {passes_per_s:.1f} passes/s wall, mean launch {ms_launch * 1e3:.1f} us, "
+        f"min {min(per_launch) * 1e3:.1f} us, max {max(per_launch) * 1e3:.1f} us")
+    traffic = load_traffic(w.name)
+    out = {
+        "metric": METRIC,
+        "value": round(passes_per_s, 2),
+        "unit": "passes/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_s / args.steps * 1e3, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
+        "data": "synthetic (seeded generator; no model weights or datasets)",
+        "config": {"workload": w.name, "seqs": w.num_seqs, "layers": w.num_layers,
+                   "kv_heads": w.num_kv_heads, "q_heads": w.num_q_heads,
+                   "head_dim": w.head_dim, "budget": w.budget[0], "block": w.block,
+                   "prompt": w.prompt[0], "n": max(states[0][3]), "variant": "l2",
+                   "running_sum": True, "parallelism": "single GPU"},
+        "kv_gbps_scanned": round(scan_gbps, 1),
+        "kv_scan_frac_of_hbm_peak": round(scan_gbps / HBM_PEAK_GBPS, 4),
+        "roofline": {"bound": "hbm", "achieved": round(alg_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(alg_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None if traffic is None else int(traffic),
+                     "traffic_over_alg": (None if traffic is None else
+                                          round(traffic / (sum(alg) / len(alg)), 3)),
+                     "kernel": "step_kernel<bf16,128,L2>",
+                     "launch_us": round(ms_launch * 1e3, 2),
+                     "alg_bytes_per_launch": int(np.mean(alg))},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the oracle on the host ...")
+        out["cpu_baseline"] = cpu_baseline(w, states[0], args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

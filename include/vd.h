@@ -1,0 +1,159 @@
+/*
+ * vd.h -- C ABI of the ValueDiff eviction pass on MI355X (gfx950).
+ *
+ * What is computed (per unit = one (sequence, layer, KV head) of a KV cache):
+ *   v_bar = (1/n) sum_{i<n} v_i over the n cached tokens, the block just
+ *           appended included (Sec. 3.2, Eq. vd; Sec. 2.2, Eq. block_processing);
+ *   score s_j (Sec. 3.2):
+ *     VD_SCORE_L2    s_j = ||v_j - v_bar||                 (Eq. vd)
+ *     VD_SCORE_DIR   s_j = 1 - cos(v_j, v_bar), with cos := 0 when
+ *                    ||v_j|| or ||v_bar|| is zero           (direction-only variant)
+ *     VD_SCORE_NORM  s_j = ||v_j||, larger kept            (magnitude-only variant)
+ *   whenever n exceeds the budget N, the N highest scores are kept
+ *   (Sec. 2.1, Eq. eviction); equal scores go to the lower slot index;
+ *   K and V are gathered onto the kept set with the slot-reuse layout:
+ *   the evicted slots below N, ascending, receive the kept slots at or above
+ *   N, ascending, so that afterwards the kept tokens occupy slots [0, N),
+ *   surviving tokens below N never move, and K, V (and pos) rows stay paired.
+ *
+ * Cache layout.  K and V share one descriptor.  Element (seq s, layer l,
+ * KV head h, slot j, channel c) lives at
+ *     base + s*stride_seq + l*stride_layer + h*stride_head + j*stride_slot + c
+ * (strides in elements; the channel stride is 1).  The usual "HND" layout
+ * [seq][layer][kv_head][slot][head_dim] and per-layer "NHD" layouts are both
+ * strides.  Rows (head_dim contiguous elements) must be 16-byte aligned.
+ * Units are numbered u = (s*num_layers + l)*num_kv_heads + h; every per-unit
+ * array below ([U][...], U = num_seqs*num_layers*num_kv_heads) is indexed so.
+ * Query heads are never read; num_q_heads is only checked for the GQA shape.
+ *
+ * Memory.  Every array pointer is a DEVICE pointer owned by the caller unless
+ * stated otherwise; n_valid and budget are HOST arrays of num_seqs entries
+ * (all units of a sequence share n and N).  The library allocates nothing
+ * and keeps no state between calls; work is queued on the caller's stream and
+ * nothing synchronizes the host.
+ *
+ * Errors.  Arguments are validated on the host before anything is queued; a
+ * rejected call returns VD_ERR_INVALID_ARG or VD_ERR_UNSUPPORTED and queues
+ * no work.  A failed launch returns VD_ERR_HIP (the HIP error stays
+ * queryable).  Device faults surface at the caller's next synchronization.
+ * Inputs must be finite; non-finite values give unspecified rankings.
+ *
+ * Precision.  Means are accumulated in fp64; scores are computed and returned
+ * in fp32, and the selection ranks exactly the fp32 values returned, so the
+ * separate and the fused paths keep the same sets.
+ */
+#ifndef VD_H
+#define VD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t;
+/* The HIP stream type (hipStream_t); NULL is the default stream. */
+typedef struct ihipStream_t *vd_stream;
+
+typedef enum {
+    VD_OK = 0,
+    VD_ERR_INVALID_ARG = 1,  /* a null, negative, inconsistent or misaligned argument */
+    VD_ERR_UNSUPPORTED = 2,  /* a valid shape this build does not handle (see limits) */
+    VD_ERR_WORKSPACE = 3,    /* workspace missing or smaller than the size query says */
+    VD_ERR_HIP = 4           /* the HIP runtime refused a launch */
+} vd_status;
+
+typedef enum { VD_DTYPE_BF16 = 0, VD_DTYPE_F32 = 1 } vd_dtype;
+
+typedef enum { VD_SCORE_L2 = 0, VD_SCORE_DIR = 1, VD_SCORE_NORM = 2 } vd_variant;
+
+/* Limits of this build. */
+#define VD_MAX_CAPACITY 16384  /* slots per unit */
+
+typedef struct {
+    void *k;               /* device; may be NULL, then only V (and pos) is gathered */
+    void *v;               /* device; never NULL */
+    int32_t dtype;         /* vd_dtype; K and V share it */
+    int32_t num_seqs;      /* >= 1 */
+    int32_t num_layers;    /* >= 1 */
+    int32_t num_kv_heads;  /* >= 1 */
+    int32_t num_q_heads;   /* multiple of num_kv_heads (GQA); otherwise unused */
+    int32_t head_dim;      /* 64, 128 or 256 */
+    int32_t capacity;      /* slots per unit, 1 .. VD_MAX_CAPACITY, >= every n_valid */
+    int64_t stride_seq, stride_layer, stride_head, stride_slot; /* elements, >= 0 */
+} vd_cache_desc;
+
+/*
+ * vd_score -- mean and scores of every unit (Sec. 3.2, Eq. vd and variants).
+ *   n_valid[s]  host; cached tokens of sequence s, 0 <= n <= capacity
+ *   scores      device float [U][capacity]; entries j < n written
+ *   mean_out    device float [U][head_dim] or NULL; the mean of units with n > 0
+ * Reads V only.  Units with n = 0 are left untouched.
+ */
+vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant variant,
+                   float *scores, float *mean_out, vd_stream stream);
+
+/*
+ * vd_select_topn -- the kept set of every unit (Sec. 2.1, Eq. eviction).
+ *   scores      device float [U][capacity], finite; first n entries read
+ *   budget[s]   host; N >= 1
+ *   keep_mask   device uint8 [U][capacity]; entry j < n set to 1 (kept) or 0
+ * Keeps the N largest scores, equal scores going to the lower slot; when
+ * n <= N every slot is kept.  -0.0 ranks as +0.0.
+ */
+vd_status vd_select_topn(const vd_cache_desc *desc, const float *scores,
+                         const int32_t *n_valid, const int32_t *budget,
+                         uint8_t *keep_mask, vd_stream stream);
+
+/*
+ * vd_compact -- slot-reuse gather of K, V and pos from a keep mask (Sec. 2.1,
+ * Eq. eviction, the gather).  For units with n > N: holes = slots j < N with
+ * keep_mask 0, ascending; movers = slots N <= j < n with keep_mask 1,
+ * ascending; the k-th mover's K row, V row and pos entry are copied onto the
+ * k-th hole.  With a mask that keeps exactly N slots this leaves the kept
+ * tokens in [0, N); with any other mask only min(#holes, #movers) rows move.
+ *   pos         device int32 [U][capacity] or NULL; a payload moved with the rows
+ */
+vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask,
+                     const int32_t *n_valid, const int32_t *budget, int32_t *pos,
+                     vd_stream stream);
+
+/*
+ * vd_evict_step -- the whole pass (mean, score, top-N, gather) of every unit
+ * in one launch: one block-processing boundary or one decode step
+ * (Sec. 2.2, Eq. block_processing).  Results equal vd_score followed by
+ * vd_select_topn and vd_compact.
+ *   n_valid[s]   host; n = tokens cached after the new block was appended
+ *   budget[s]    host; N >= 1; units with n <= N keep everything
+ *   running_sum  device double [U][head_dim + 1] or NULL.  Optional state
+ *                that spares re-reading the old rows for the mean: entries
+ *                0..head_dim-1 hold the sum of the unit's cached value rows
+ *                [0, count) and entry head_dim holds count.  On entry, rows
+ *                [count, n) are taken as new (count outside [0, n] means
+ *                "recompute from all n rows"); on return the state describes
+ *                the cache after the pass (count = min(n, N)).  Zero-filled
+ *                memory is a valid empty state.  The caller must not change
+ *                rows [0, count) between calls without resetting the state.
+ *   pos          device int32 [U][capacity] or NULL; moved with the rows
+ *   scores_out   device float [U][capacity] or NULL; the scores, j < n
+ *   keep_out     device uint8 [U][capacity] or NULL; the keep mask, j < n
+ *   workspace    may be NULL when vd_evict_step_workspace_size() returns 0
+ * After the call the caller sets n_valid[s] = min(n, N).
+ */
+vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid,
+                        const int32_t *budget, vd_variant variant, double *running_sum,
+                        int32_t *pos, float *scores_out, uint8_t *keep_out,
+                        void *workspace, size_t workspace_bytes, vd_stream stream);
+
+/* Bytes of device workspace vd_evict_step needs for this descriptor (0 in this build). */
+size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);
+
+/* A static description of a status code. */
+const char *vd_status_string(vd_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VD_H */

@@ -1,0 +1,248 @@
+// Host side of the C ABI declared in include/vd.h: argument validation (before
+// anything touches the GPU), the per-launch LDS plan, and the launches on the
+// caller's stream.  Sequences are processed in launches of at most
+// kMaxSeqsPerLaunch, whose n and N travel as kernel arguments.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+
+#include "vd.h"
+#include "vd_launch.h"
+
+namespace {
+
+using vd::UnitParams;
+
+int64_t elem_bytes(int32_t dtype) { return dtype == VD_DTYPE_BF16 ? 2 : 4; }
+int64_t align16(int64_t x) { return (x + 15) & ~int64_t(15); }
+bool aligned(const void *p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+vd_status check_desc(const vd_cache_desc *d) {
+    if (!d || !d->v) return VD_ERR_INVALID_ARG;
+    if (d->dtype != VD_DTYPE_BF16 && d->dtype != VD_DTYPE_F32) return VD_ERR_INVALID_ARG;
+    if (d->num_seqs < 1 || d->num_layers < 1 || d->num_kv_heads < 1 || d->num_q_heads < 1)
+        return VD_ERR_INVALID_ARG;
+    if (d->num_q_heads % d->num_kv_heads != 0) return VD_ERR_INVALID_ARG;
+    if (d->head_dim < 1 || d->capacity < 1) return VD_ERR_INVALID_ARG;
+    if (d->head_dim != 64 && d->head_dim != 128 && d->head_dim != 256) return VD_ERR_UNSUPPORTED;
+    if (d->capacity > VD_MAX_CAPACITY) return VD_ERR_UNSUPPORTED;
+    if (d->stride_seq < 0 || d->stride_layer < 0 || d->stride_head < 0 || d->stride_slot < 0)
+        return VD_ERR_INVALID_ARG;
+    if (d->stride_slot < d->head_dim) return VD_ERR_INVALID_ARG;  // rows would overlap
+    const int64_t units = int64_t(d->num_seqs) * d->num_layers * d->num_kv_heads;
+    if (units > INT32_MAX || units * int64_t(d->capacity) > (int64_t(1) << 47))
+        return VD_ERR_UNSUPPORTED;
+    const int64_t es = elem_bytes(d->dtype);
+    const int64_t strides[4] = {d->stride_seq, d->stride_layer, d->stride_head, d->stride_slot};
+    for (int64_t s : strides)
+        if ((s * es) % 16 != 0) return VD_ERR_INVALID_ARG;  // every row 16-byte aligned
+    if (!aligned(d->v, 16) || (d->k && !aligned(d->k, 16))) return VD_ERR_INVALID_ARG;
+    if (d->k && d->k == d->v) return VD_ERR_INVALID_ARG;
+    return VD_OK;
+}
+
+vd_status check_counts(const vd_cache_desc *d, const int32_t *n_valid, const int32_t *budget) {
+    if (!n_valid) return VD_ERR_INVALID_ARG;
+    for (int s = 0; s < d->num_seqs; ++s) {
+        if (n_valid[s] < 0 || n_valid[s] > d->capacity) return VD_ERR_INVALID_ARG;
+        if (budget && budget[s] < 1) return VD_ERR_INVALID_ARG;
+    }
+    return VD_OK;
+}
+
+UnitParams base_params(const vd_cache_desc *d, int s0, int ns, const int32_t *n_valid,
+                       const int32_t *budget) {
+    UnitParams p;
+    std::memset(&p, 0, sizeof p);
+    const int64_t es = elem_bytes(d->dtype);
+    p.k = d->k ? static_cast<char *>(d->k) + int64_t(s0) * d->stride_seq * es : nullptr;
+    p.v = static_cast<char *>(d->v) + int64_t(s0) * d->stride_seq * es;
+    p.s_seq = d->stride_seq * es;
+    p.s_layer = d->stride_layer * es;
+    p.s_head = d->stride_head * es;
+    p.s_slot = d->stride_slot * es;
+    p.num_layers = d->num_layers;
+    p.num_kv_heads = d->num_kv_heads;
+    p.unit0 = s0 * d->num_layers * d->num_kv_heads;
+    p.capacity = d->capacity;
+    for (int i = 0; i < ns; ++i) {
+        p.n[i] = n_valid[s0 + i];
+        p.N[i] = budget ? budget[s0 + i] : INT32_MAX;
+    }
+    return p;
+}
+
+// Plans the dynamic LDS of the pass kernel for one launch.
+vd_status plan_step_lds(const vd_cache_desc *d, UnitParams &p, int ns, bool score_mode,
+                        bool have_state, size_t &lds_bytes) {
+    const int64_t row_bytes = int64_t(d->head_dim) * elem_bytes(d->dtype);
+    int nmax = 0, keys_cap = 0, evict_cap = 0, move_cap = 0, want_rows = 0;
+    for (int i = 0; i < ns; ++i) {
+        const int n = p.n[i], N = p.N[i];
+        nmax = std::max(nmax, n);
+        if (!score_mode && n > N) {
+            if (n > N + 1) keys_cap = std::max(keys_cap, n);
+            evict_cap = std::max(evict_cap, n - N);
+            move_cap = std::max(move_cap, std::min(N, n - N));
+            want_rows = std::max(want_rows, have_state ? n - N : n);
+        } else if (!have_state) {
+            want_rows = std::max(want_rows, n);
+        }
+    }
+    const int64_t red_bytes = int64_t(vd::kWaves) * d->head_dim * 8;
+    const int64_t keys_bytes = align16(std::max<int64_t>(int64_t(keys_cap) * 4, red_bytes));
+    const int64_t lists_bytes = align16(int64_t(evict_cap + move_cap) * 4);
+    const int64_t used = int64_t(sizeof(vd::LdsHead)) + keys_bytes + lists_bytes;
+    if (used > vd::kLdsBytes) return VD_ERR_UNSUPPORTED;
+    const int64_t stash_rows = (int64_t(want_rows) * row_bytes <= vd::kLdsBytes - used) ? want_rows : 0;
+    p.off_keys = int32_t(sizeof(vd::LdsHead));
+    p.off_lists = int32_t(p.off_keys + keys_bytes);
+    p.off_stash = int32_t(p.off_lists + lists_bytes);
+    p.keys_cap = keys_cap;
+    p.evict_cap = evict_cap;
+    p.move_cap = move_cap;
+    p.stash_rows = int32_t(stash_rows);
+    lds_bytes = size_t(used + stash_rows * row_bytes);
+    return VD_OK;
+}
+
+vd_status launched(hipError_t e) { return e == hipSuccess ? VD_OK : VD_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant variant,
+                   float *scores, float *mean_out, vd_stream stream) {
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if ((st = check_counts(desc, n_valid, nullptr)) != VD_OK) return st;
+    if (variant < VD_SCORE_L2 || variant > VD_SCORE_NORM) return VD_ERR_INVALID_ARG;
+    if (!scores || !aligned(scores, 4) || (mean_out && !aligned(mean_out, 4)))
+        return VD_ERR_INVALID_ARG;
+    const int per_seq = desc->num_layers * desc->num_kv_heads;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
+        const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, nullptr);
+        p.mode = vd::kModeScore;
+        p.scores = scores;
+        p.mean_out = mean_out;
+        size_t lds = 0;
+        if ((st = plan_step_lds(desc, p, ns, true, false, lds)) != VD_OK) return st;
+        st = launched(vd::launch_step(p, ns * per_seq, desc->dtype, desc->head_dim, variant, lds,
+                                      reinterpret_cast<hipStream_t>(stream)));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
+}
+
+vd_status vd_select_topn(const vd_cache_desc *desc, const float *scores, const int32_t *n_valid,
+                         const int32_t *budget, uint8_t *keep_mask, vd_stream stream) {
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if (!budget) return VD_ERR_INVALID_ARG;
+    if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
+    if (!scores || !keep_mask || !aligned(scores, 4)) return VD_ERR_INVALID_ARG;
+    const int per_seq = desc->num_layers * desc->num_kv_heads;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
+        const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, budget);
+        p.scores_in = scores;
+        p.keep = keep_mask;
+        int nmax = 0;
+        for (int i = 0; i < ns; ++i) nmax = std::max(nmax, p.n[i]);
+        p.off_keys = int32_t(sizeof(vd::LdsHead));
+        p.keys_cap = nmax;
+        const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(nmax) * 4));
+        if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
+        st = launched(vd::launch_select(p, ns * per_seq, lds, reinterpret_cast<hipStream_t>(stream)));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
+}
+
+vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask, const int32_t *n_valid,
+                     const int32_t *budget, int32_t *pos, vd_stream stream) {
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if (!budget) return VD_ERR_INVALID_ARG;
+    if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
+    if (!keep_mask || (pos && !aligned(pos, 4))) return VD_ERR_INVALID_ARG;
+    const int per_seq = desc->num_layers * desc->num_kv_heads;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
+        const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, budget);
+        p.keep_in = keep_mask;
+        p.pos = pos;
+        int holes = 0, movers = 0;
+        for (int i = 0; i < ns; ++i) {
+            if (p.n[i] > p.N[i]) {
+                holes = std::max(holes, std::min(p.N[i], p.n[i]));
+                movers = std::max(movers, p.n[i] - p.N[i]);
+            }
+        }
+        if (holes == 0) continue;  // nothing exceeds its budget in this launch
+        p.off_lists = int32_t(sizeof(vd::LdsHead));
+        p.evict_cap = holes;
+        p.move_cap = movers;
+        const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(holes + movers) * 4));
+        if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
+        st = launched(vd::launch_compact(p, ns * per_seq, desc->dtype, desc->head_dim, lds,
+                                         reinterpret_cast<hipStream_t>(stream)));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
+}
+
+vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const int32_t *budget,
+                        vd_variant variant, double *running_sum, int32_t *pos, float *scores_out,
+                        uint8_t *keep_out, void *workspace, size_t workspace_bytes,
+                        vd_stream stream) {
+    (void)workspace;
+    (void)workspace_bytes;
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if (!budget) return VD_ERR_INVALID_ARG;
+    if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
+    if (variant < VD_SCORE_L2 || variant > VD_SCORE_NORM) return VD_ERR_INVALID_ARG;
+    if ((running_sum && !aligned(running_sum, 8)) || (pos && !aligned(pos, 4)) ||
+        (scores_out && !aligned(scores_out, 4)))
+        return VD_ERR_INVALID_ARG;
+    const int per_seq = desc->num_layers * desc->num_kv_heads;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
+        const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, budget);
+        p.mode = vd::kModeStep;
+        p.running_sum = running_sum;
+        p.pos = pos;
+        p.scores = scores_out;
+        p.keep = keep_out;
+        size_t lds = 0;
+        if ((st = plan_step_lds(desc, p, ns, false, running_sum != nullptr, lds)) != VD_OK)
+            return st;
+        st = launched(vd::launch_step(p, ns * per_seq, desc->dtype, desc->head_dim, variant, lds,
+                                      reinterpret_cast<hipStream_t>(stream)));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
+}
+
+size_t vd_evict_step_workspace_size(const vd_cache_desc *desc) {
+    (void)desc;
+    return 0;
+}
+
+const char *vd_status_string(vd_status status) {
+    switch (status) {
+        case VD_OK: return "ok";
+        case VD_ERR_INVALID_ARG: return "invalid argument";
+        case VD_ERR_UNSUPPORTED: return "unsupported shape";
+        case VD_ERR_WORKSPACE: return "workspace missing or too small";
+        case VD_ERR_HIP: return "HIP launch failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

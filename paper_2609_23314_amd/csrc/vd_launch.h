@@ -1,0 +1,64 @@
+// Internal contract between the host entry points (vd_api.cpp) and the
+// kernels (vd_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace vd {
+
+constexpr int kBlock = 1024;              // threads per workgroup (16 waves of 64)
+constexpr int kWaves = kBlock / 64;
+constexpr int kMaxSeqsPerLaunch = 256;    // per-sequence n and N travel as kernel arguments
+constexpr int kLdsBytes = 160 * 1024;     // LDS of one gfx950 workgroup
+
+enum Mode : int32_t { kModeStep = 0, kModeScore = 1 };
+
+// Fixed head of the dynamic LDS of every kernel.
+struct LdsHead {
+    uint32_t bc[128];     // broadcast slots and per-wave partials
+    uint32_t hist[256];   // radix histogram
+    float mean[256];      // fp32 mean used for scoring
+    float udir[256];      // mean / ||mean|| (direction variant)
+    double sum[256];      // fp64 column sums
+    double sum_ev[256];   // fp64 column sums of the evicted rows
+};
+static_assert(sizeof(LdsHead) % 16 == 0, "LDS head must keep 16-byte alignment");
+
+struct UnitParams {
+    char *k;                  // first unit of the launch's first sequence; may be null
+    char *v;
+    int64_t s_seq, s_layer, s_head, s_slot;   // strides in BYTES
+    int32_t num_layers, num_kv_heads;
+    int32_t unit0;            // global index of the launch's first unit
+    int32_t capacity;
+    int32_t mode;             // Mode
+    int32_t pad0;
+    double *running_sum;      // [U][D+1] or null
+    int32_t *pos;             // [U][capacity] or null
+    float *scores;            // [U][capacity] or null (required in kModeScore)
+    const float *scores_in;   // select kernel input
+    uint8_t *keep;            // [U][capacity] or null (output of step/select)
+    const uint8_t *keep_in;   // compact kernel input
+    float *mean_out;          // [U][D] or null
+    // dynamic LDS layout (byte offsets from the start of dynamic LDS)
+    int32_t off_keys;         // keys / fp64 reduction scratch
+    int32_t off_lists;        // evicted (or hole) list, then mover list
+    int32_t off_stash;        // staged rows
+    int32_t keys_cap;         // entries in the keys region
+    int32_t evict_cap;        // entries of the first list
+    int32_t move_cap;         // entries of the second list
+    int32_t stash_rows;       // rows the stash holds
+    int32_t pad1;
+    int32_t n[kMaxSeqsPerLaunch];
+    int32_t N[kMaxSeqsPerLaunch];
+};
+
+hipError_t launch_step(const UnitParams &p, int num_units, int dtype, int head_dim,
+                       int variant, size_t lds_bytes, hipStream_t stream);
+hipError_t launch_select(const UnitParams &p, int num_units, size_t lds_bytes,
+                         hipStream_t stream);
+hipError_t launch_compact(const UnitParams &p, int num_units, int dtype, int head_dim,
+                          size_t lds_bytes, hipStream_t stream);
+
+}  // namespace vd

@@ -1,0 +1,113 @@
+"""The C ABI on the host: the library loads, exports every entry point that
+include/vd.h declares, and rejects bad arguments before touching the GPU
+(these calls return before any HIP call, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_23314_amd import vd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vd.h")
+
+FAKE_V = 0x7F0000000000   # never dereferenced: validation fails first
+FAKE_K = 0x7F0000100000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:vd_status|size_t|const char \*)\s*(vd_\w+)\s*\(",
+                                 text, flags=re.M)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for f in ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step"):
+        assert f in names
+    assert set(names) == set(vd.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(vd.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def good_desc(**kw):
+    d = vd.VdCacheDesc()
+    d.k, d.v = FAKE_K, FAKE_V
+    d.dtype = vd.VD_DTYPE_BF16
+    d.num_seqs, d.num_layers, d.num_kv_heads, d.num_q_heads = 2, 3, 4, 16
+    d.head_dim, d.capacity = 128, 100
+    d.stride_slot = 128
+    d.stride_head = 100 * 128
+    d.stride_layer = 4 * 100 * 128
+    d.stride_seq = 3 * 4 * 100 * 128
+    for k, v in kw.items():
+        setattr(d, k, v)
+    return d
+
+
+def call_step(d, n=(50, 60), N=(40, 40), variant=0, rs=None, **kw):
+    lib = vd.load()
+    S = max(int(d.num_seqs), 1)
+    n_arr = (ctypes.c_int32 * S)(*(list(n) + [0] * S)[:S])
+    N_arr = (ctypes.c_int32 * S)(*(list(N) + [1] * S)[:S])
+    return lib.vd_evict_step(ctypes.byref(d), n_arr, N_arr, variant, rs, None, None, None, None,
+                             0, None)
+
+
+@pytest.mark.parametrize("field,value,status", [
+    ("v", None, vd.VD_ERR_INVALID_ARG),
+    ("dtype", 7, vd.VD_ERR_INVALID_ARG),
+    ("num_seqs", 0, vd.VD_ERR_INVALID_ARG),
+    ("num_layers", -1, vd.VD_ERR_INVALID_ARG),
+    ("num_q_heads", 6, vd.VD_ERR_INVALID_ARG),      # not a multiple of the KV heads
+    ("head_dim", 96, vd.VD_ERR_UNSUPPORTED),
+    ("head_dim", 0, vd.VD_ERR_INVALID_ARG),
+    ("capacity", 0, vd.VD_ERR_INVALID_ARG),
+    ("capacity", vd.MAX_CAPACITY + 1, vd.VD_ERR_UNSUPPORTED),
+    ("stride_slot", 64, vd.VD_ERR_INVALID_ARG),     # rows would overlap
+    ("stride_slot", 132, vd.VD_ERR_INVALID_ARG),    # rows not 16-byte aligned
+    ("stride_head", -128, vd.VD_ERR_INVALID_ARG),
+    ("v", FAKE_V + 8, vd.VD_ERR_INVALID_ARG),       # misaligned base
+    ("k", FAKE_V, vd.VD_ERR_INVALID_ARG),           # k aliases v
+])
+def test_descriptor_rejected(field, value, status):
+    assert call_step(good_desc(**{field: value})) == status
+
+
+def test_counts_rejected():
+    d = good_desc()
+    assert call_step(d, n=(101, 5)) == vd.VD_ERR_INVALID_ARG    # n > capacity
+    assert call_step(d, n=(-1, 5)) == vd.VD_ERR_INVALID_ARG
+    assert call_step(d, N=(0, 5)) == vd.VD_ERR_INVALID_ARG      # budget < 1
+    assert call_step(d, variant=3) == vd.VD_ERR_INVALID_ARG
+    assert call_step(d, rs=ctypes.c_void_p(0x1004)) == vd.VD_ERR_INVALID_ARG  # misaligned state
+    lib = vd.load()
+    n_arr = (ctypes.c_int32 * 2)(5, 5)
+    assert lib.vd_evict_step(ctypes.byref(d), n_arr, None, 0, None, None, None, None, None, 0,
+                             None) == vd.VD_ERR_INVALID_ARG     # budget missing
+    assert lib.vd_score(ctypes.byref(d), n_arr, 0, None, None, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_select_topn(ctypes.byref(d), None, n_arr, n_arr, None, None) == \
+        vd.VD_ERR_INVALID_ARG
+    assert lib.vd_compact(ctypes.byref(d), None, n_arr, n_arr, None, None) == \
+        vd.VD_ERR_INVALID_ARG
+    assert lib.vd_evict_step(None, n_arr, n_arr, 0, None, None, None, None, None, 0, None) == \
+        vd.VD_ERR_INVALID_ARG
+
+
+def test_status_strings_and_workspace():
+    lib = vd.load()
+    for s in range(5):
+        assert lib.vd_status_string(s)
+    assert lib.vd_evict_step_workspace_size(ctypes.byref(good_desc())) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(vd, "_lib", None)
+    monkeypatch.setattr(vd, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        vd.load()
