@@ -9,15 +9,22 @@
 //
 //   mean    fp64 column sums of the rows not yet summed (all n, or only the
 //           appended rows when the caller keeps a running sum), reduced in a
-//           fixed order                                     (Sec. 3.2, Eq. vd)
+//           fixed order; the first tile of old rows is already in flight
+//                                                        (Sec. 3.2, Eq. vd)
 //   score   fp32, one DPP row reduction per row (two for Dir)  (Sec. 3.2)
-//   select  radix select of the N-th largest fp32 score on its order-
-//           preserving uint32 key, ties to the lower slot; a single block
-//           argmin when exactly one token goes (decode)  (Sec. 2.1, Eq. eviction)
+//   select  the N-th largest fp32 score on its order-preserving uint32 key:
+//           a histogram over the key range narrows it to one bin, whose few
+//           keys one wave ranks exactly; ties go to the lower slot; a single
+//           block argmin when exactly one token goes (decode)
+//                                                 (Sec. 2.1, Eq. eviction)
 //   gather  slot reuse: evicted slots below N, ascending, receive the kept
-//           slots at or above N, ascending; only those rows move
+//           slots at or above N, ascending; only those rows move; the same
+//           loop reads the evicted rows for the running-sum update
 //
-// No MFMA: nothing here is a dense contraction.
+// Row streams are software-pipelined: the loads of tile t+1 are in flight
+// while tile t is reduced, and every lane loads unconditionally (rows past
+// the end are clamped to the last row and ignored).  No MFMA: nothing here is
+// a dense contraction.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -28,7 +35,8 @@ namespace {
 
 constexpr int NT = kBlock;
 constexpr int NW = kWaves;
-constexpr int kUnroll = 8;  // 16-byte loads in flight per lane in the row streams
+constexpr int kUnroll = 4;  // 16-byte loads per lane per tile (two tiles in flight)
+static_assert(NT == kBins, "the selection gives every thread one histogram bin");
 
 // ---------------------------------------------------------------- elements
 
@@ -56,6 +64,7 @@ template <int DT, int D> struct Shape {
     static constexpr int LPR = ROWB / 16;             // lanes per row
     static constexpr int RPW = 64 / LPR;              // rows per wave instruction
     static constexpr int GROUPS = NW * RPW;           // row groups per workgroup
+    static constexpr int STEP = GROUPS * kUnroll;     // rows per tile
     static_assert(LPR >= 1 && LPR <= 64 && 64 % LPR == 0, "unsupported row shape");
 };
 
@@ -63,6 +72,7 @@ template <int DT, int D> struct Shape {
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & 63; }
 __device__ __forceinline__ int wave_id() { return threadIdx.x >> 6; }
+__device__ __forceinline__ uint64_t lanes_below() { return (1ull << lane_id()) - 1ull; }
 
 template <int CTRL> __device__ __forceinline__ float dpp(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
@@ -103,52 +113,68 @@ __device__ __forceinline__ uint32_t orderable(float f) {
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
 }
 
-// Exclusive rank of `flag` among the block's threads in thread order, and the
-// block-wide count.  Two barriers; `wsum` holds NW entries.
-__device__ __forceinline__ uint32_t block_rank(bool flag, uint32_t *wsum, uint32_t &total) {
-    const uint64_t m = __ballot(flag);
-    const int lane = lane_id(), w = wave_id();
-    const uint32_t in_wave = __popcll(m & ((1ull << lane) - 1ull));
-    if (lane == 0) wsum[w] = __popcll(m);
-    __syncthreads();
-    uint32_t before = 0, tot = 0;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-        const uint32_t c = wsum[i];
-        before += (i < w) ? c : 0u;
-        tot += c;
-    }
-    __syncthreads();
-    total = tot;
-    return before + in_wave;
-}
-
 // ---------------------------------------------------------------- row streams
 
-// Streams `count` rows: element e (0 <= e < count) is row row_of(e), fetched
-// 16 bytes per lane by fetch(row, chunk); body(e, valid, data) runs on every
-// lane (lanes past the end see zeros and valid == false), so DPP reductions
-// inside body always see full row groups.  kUnroll loads are issued before the
-// first use.
+// Tile t of a stream of `count` rows: slot k of this lane is element
+// t*STEP + (k*NW + wave)*RPW + lane/LPR; row_of maps an element to a row and
+// fetch(row, chunk) returns the lane's 16 bytes of it.
+template <int DT, int D, typename RowOf, typename Fetch>
+__device__ __forceinline__ void load_tile(int t, int count, RowOf row_of, Fetch fetch,
+                                          uint4 (&buf)[kUnroll]) {
+    using S = Shape<DT, D>;
+    const int base = t * S::STEP + wave_id() * S::RPW + lane_id() / S::LPR;
+    const int cl = lane_id() % S::LPR;
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+        const int e = base + k * NW * S::RPW;
+        buf[k] = fetch(row_of(e < count ? e : count - 1), cl);
+    }
+}
+
+template <int DT, int D, typename Body>
+__device__ __forceinline__ void use_tile(int t, int count, const uint4 (&buf)[kUnroll], Body body) {
+    using S = Shape<DT, D>;
+    const int base = t * S::STEP + wave_id() * S::RPW + lane_id() / S::LPR;
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+        const int e = base + k * NW * S::RPW;
+        body(e, e < count, buf[k]);
+    }
+}
+
+// Streams elements [0, count) whose tiles 0 and 1 are already loaded in `a`
+// and `b` (tile 1 only if it exists); body(e, valid, data) runs on every
+// lane, so DPP reductions inside it always see whole row groups.
+template <int DT, int D, typename RowOf, typename Fetch, typename Body>
+__device__ __forceinline__ void for_rows_pre2(int count, RowOf row_of, Fetch fetch, Body body,
+                                              uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
+    using S = Shape<DT, D>;
+    const int ntiles = (count + S::STEP - 1) / S::STEP;
+    int t = 0;
+    for (; t + 1 < ntiles; t += 2) {
+        use_tile<DT, D>(t, count, a, body);
+        if (t + 2 < ntiles) load_tile<DT, D>(t + 2, count, row_of, fetch, a);
+        use_tile<DT, D>(t + 1, count, b, body);
+        if (t + 3 < ntiles) load_tile<DT, D>(t + 3, count, row_of, fetch, b);
+    }
+    if (t < ntiles) use_tile<DT, D>(t, count, a, body);
+}
+
+// Loads the first two tiles of a stream (the second only if it exists).
+template <int DT, int D, typename RowOf, typename Fetch>
+__device__ __forceinline__ void load_first2(int count, RowOf row_of, Fetch fetch,
+                                            uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
+    using S = Shape<DT, D>;
+    load_tile<DT, D>(0, count, row_of, fetch, a);
+    if (count > S::STEP) load_tile<DT, D>(1, count, row_of, fetch, b);
+}
+
 template <int DT, int D, typename RowOf, typename Fetch, typename Body>
 __device__ __forceinline__ void for_rows(int count, RowOf row_of, Fetch fetch, Body body) {
-    using S = Shape<DT, D>;
-    const int lane = lane_id(), w = wave_id();
-    const int q = lane / S::LPR, cl = lane % S::LPR;
-    constexpr int STEP = S::GROUPS * kUnroll;
-    for (int e0 = 0; e0 < count; e0 += STEP) {
-        uint4 buf[kUnroll];
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int e = e0 + (k * NW + w) * S::RPW + q;
-            buf[k] = e < count ? fetch(row_of(e), cl) : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-        for (int k = 0; k < kUnroll; ++k) {
-            const int e = e0 + (k * NW + w) * S::RPW + q;
-            body(e, e < count, buf[k]);
-        }
-    }
+    if (count <= 0) return;
+    uint4 a[kUnroll], b[kUnroll];
+    load_first2<DT, D>(count, row_of, fetch, a, b);
+    for_rows_pre2<DT, D>(count, row_of, fetch, body, a, b);
 }
 
 // Column sums of per-lane fp64 partials (each lane holds EPL columns of its
@@ -182,15 +208,15 @@ struct Threshold {
     int count_eq;      // how many keys equal `key`
 };
 
-// Radix select of the N-th largest of keys[0..n) (1 <= N < n), MSB first,
-// 8-bit digits starting at the highest bit in which the keys differ.
-__device__ Threshold radix_select(const uint32_t *keys, int n, int N, LdsHead &H) {
-    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-    for (int j = threadIdx.x; j < n; j += NT) {
-        const uint32_t k = keys[j];
-        kmin = min(kmin, k);
-        kmax = max(kmax, k);
-    }
+// The N-th largest of keys[0..n) (1 <= N < n).  Each pass histograms the keys
+// still in play, bin = (key - lo) >> shift with shift chosen so that the range
+// [lo, hi] fills at most kBins bins, and keeps the bin holding the N-th
+// largest; once a bin holds at most kCand keys, one wave ranks them by
+// (key desc, slot asc).  A pass narrows the range 512-fold or more, so at most
+// four passes run.
+// kmin / kmax are this thread's partial minimum and maximum of the keys.
+__device__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32_t kmin,
+                                      uint32_t kmax, LdsHead &H) {
     kmin = wave_min_u32(kmin);
     kmax = wave_max_u32(kmax);
     if (lane_id() == 0) {
@@ -198,101 +224,170 @@ __device__ Threshold radix_select(const uint32_t *keys, int n, int N, LdsHead &H
         H.bc[32 + wave_id()] = kmax;
     }
     __syncthreads();
-    kmin = H.bc[0];
-    kmax = H.bc[32];
+    uint32_t lo = H.bc[0], hi = H.bc[32];
 #pragma unroll
     for (int i = 1; i < NW; ++i) {
-        kmin = min(kmin, H.bc[i]);
-        kmax = max(kmax, H.bc[32 + i]);
+        lo = min(lo, H.bc[i]);
+        hi = max(hi, H.bc[32 + i]);
     }
     __syncthreads();
-    if (kmin == kmax) return Threshold{kmin, N, n};
-
-    const int hb = 31 - __clz(kmin ^ kmax);
-    uint32_t prefix = hb == 31 ? 0u : (kmin & ~((2u << hb) - 1u));
     int need = N;
-    int top = hb;
-    int count_in_bin = 0;
+    int in_range = n;
     for (;;) {
-        const int width = top + 1 < 8 ? top + 1 : 8;
-        const int shift = top + 1 - width;
-        const uint32_t hi_mask = top == 31 ? 0u : ~((2u << top) - 1u);
-        const uint32_t dmask = (1u << width) - 1u;
-        for (int i = threadIdx.x; i < 256; i += NT) H.hist[i] = 0u;
+        if (lo == hi) return Threshold{lo, need, in_range};
+        const int bits = 32 - __clz(hi - lo);   // bits of the largest offset
+        const int shift = bits > 10 ? bits - 10 : 0;
+        H.hist[threadIdx.x] = 0u;  // NT == kBins
+        if (threadIdx.x == 0) H.bc[100] = 0u;
         __syncthreads();
         for (int j = threadIdx.x; j < n; j += NT) {
             const uint32_t k = keys[j];
-            if ((k & hi_mask) == prefix) atomicAdd(&H.hist[(k >> shift) & dmask], 1u);
+            if (k >= lo && k <= hi) atomicAdd(&H.hist[(k - lo) >> shift], 1u);
+        }
+        __syncthreads();
+        // suffix sums over the bins: thread t owns bin t
+        const uint32_t h = H.hist[threadIdx.x];
+        uint32_t suf = h;
+        for (int o = 1; o < 64; o <<= 1) {
+            const uint32_t v = __shfl_down(suf, o);
+            if (lane_id() + o < 64) suf += v;
+        }
+        if (lane_id() == 0) H.bc[wave_id()] = suf;  // wave totals
+        __syncthreads();
+        uint32_t above = suf - h;
+        for (int i = wave_id() + 1; i < NW; ++i) above += H.bc[i];
+        const uint32_t un = (uint32_t)need;
+        if (above < un && un <= above + h) {
+            H.bc[64] = threadIdx.x;
+            H.bc[65] = above;
+            H.bc[66] = h;
+        }
+        __syncthreads();
+        const uint64_t b = H.bc[64];
+        need -= (int)H.bc[65];
+        in_range = (int)H.bc[66];
+        const uint64_t top = (uint64_t)lo + ((b + 1) << shift) - 1u;
+        hi = top < (uint64_t)hi ? (uint32_t)top : hi;
+        lo = lo + (uint32_t)(b << shift);
+        if (lo == hi || in_range > kCand) {
+            __syncthreads();
+            continue;
+        }
+        // few keys left: gather them and rank them exactly
+        for (int j = threadIdx.x; j < n; j += NT) {
+            const uint32_t k = keys[j];
+            if (k >= lo && k <= hi) {
+                const uint32_t slot = atomicAdd(&H.bc[100], 1u);
+                H.cand_key[slot] = k;
+                H.cand_idx[slot] = (uint32_t)j;
+            }
         }
         __syncthreads();
         if (wave_id() == 0) {
-            // lane l owns bins 4l..4l+3; find bin b with above(b) < need <= above(b) + hist[b]
-            const int l = lane_id();
-            const uint32_t h0 = H.hist[4 * l], h1 = H.hist[4 * l + 1];
-            const uint32_t h2 = H.hist[4 * l + 2], h3 = H.hist[4 * l + 3];
-            const uint32_t local = h0 + h1 + h2 + h3;
-            uint32_t suf = local;  // inclusive suffix sum over lanes
-            for (int o = 1; o < 64; o <<= 1) {
-                const uint32_t t = __shfl_down(suf, o);
-                if (l + o < 64) suf += t;
+            const int c = in_range;
+            const int i = lane_id();
+            const uint32_t ki = i < c ? H.cand_key[i] : 0u;
+            const uint32_t ji = i < c ? H.cand_idx[i] : 0u;
+            int rank = 0;
+            for (int t = 0; t < c; ++t) {  // t is wave-uniform: operands come by readlane
+                const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)ki, t);
+                const uint32_t jt = (uint32_t)__builtin_amdgcn_readlane((int)ji, t);
+                rank += (kt > ki || (kt == ki && jt < ji)) ? 1 : 0;
             }
-            uint32_t above = suf - local;
-            const uint32_t hh[4] = {h0, h1, h2, h3};
-            const uint32_t un = (uint32_t)need;
-#pragma unroll
-            for (int t = 3; t >= 0; --t) {
-                if (above < un && un <= above + hh[t]) {
-                    H.bc[64] = 4u * l + t;
-                    H.bc[65] = above;
-                    H.bc[66] = hh[t];
-                }
-                above += hh[t];
+            if (i >= c) rank = -1;
+            // the candidate ranked need-1 fixes the threshold key
+            const uint64_t m = __ballot(rank == need - 1);
+            const int src = __ffsll((unsigned long long)m) - 1;
+            const uint32_t T = __shfl(ki, src);
+            const uint32_t n_gt = __popcll(__ballot(i < c && ki > T));
+            const uint32_t n_eq = __popcll(__ballot(i < c && ki == T));
+            if (i == 0) {
+                H.bc[67] = T;
+                H.bc[68] = (uint32_t)need - n_gt;
+                H.bc[69] = n_eq;
             }
         }
         __syncthreads();
-        const uint32_t b = H.bc[64];
-        need -= (int)H.bc[65];
-        count_in_bin = (int)H.bc[66];
+        const Threshold th{H.bc[67], (int)H.bc[68], (int)H.bc[69]};
         __syncthreads();
-        prefix |= b << shift;
-        if (shift == 0) break;
-        top = shift - 1;
+        return th;
     }
-    return Threshold{prefix, need, count_in_bin};
 }
 
-// Walks slots [0, n) in block-sized chunks and decides keep(j) from the
-// threshold; appends evicted slots (ascending) to evl and kept slots >= N
-// (ascending) to mvl; writes keep_out if given.  Returns the mover count.
+// Decides keep(j) for j < n from the threshold and appends the evicted slots
+// (ascending) to evl and the kept slots >= N (ascending) to mvl; writes
+// keep_out if given.  Wave w owns a contiguous segment of slots, so only the
+// per-wave counts cross waves.  Returns the number of movers.
 __device__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &th,
                            uint32_t *evl, int evict_cap, uint32_t *mvl, int move_cap,
                            uint8_t *keep_out, LdsHead &H) {
-    uint32_t eq_off = 0, ev_off = 0, mv_off = 0;
+    const int w = wave_id(), lane = lane_id();
+    const int seg = (((n + NW - 1) / NW) + 63) & ~63;
+    const int j0 = w * seg;
+    const int j1 = min(n, j0 + seg);
     const bool rank_eq = th.count_eq != th.need;
-    for (int base = 0; base < n; base += NT) {
-        const int j = base + threadIdx.x;
-        const bool valid = j < n;
-        const uint32_t k = valid ? keys[j] : 0u;
-        const bool gt = valid && k > th.key;
-        const bool eq = valid && k == th.key;
-        bool keep = gt || eq;
-        if (rank_eq) {
-            uint32_t tot;
-            const uint32_t r = block_rank(eq, H.bc, tot) + eq_off;
-            eq_off += tot;
-            keep = gt || (eq && r < (uint32_t)th.need);
+    const uint32_t T = th.key;
+    uint32_t eq_before = 0;
+    if (rank_eq) {
+        uint32_t c = 0;
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            c += __popcll(__ballot(j < j1 && keys[j] == T));
         }
-        uint32_t tot_ev, tot_mv;
-        const uint32_t rev = block_rank(valid && !keep, H.bc, tot_ev) + ev_off;
-        const uint32_t rmv = block_rank(valid && keep && j >= N, H.bc, tot_mv) + mv_off;
-        if (valid && !keep && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
-        if (valid && keep && j >= N && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
-        if (keep_out && valid) keep_out[j] = keep ? 1 : 0;
-        ev_off += tot_ev;
-        mv_off += tot_mv;
+        if (lane == 0) H.bc[w] = c;
+        __syncthreads();
+        for (int i = 0; i < w; ++i) eq_before += H.bc[i];
+        __syncthreads();
+    }
+    auto decide = [&](int j, bool valid, uint32_t &eqr) -> bool {
+        const uint32_t k = valid ? keys[j] : 0u;
+        const bool gt = valid && k > T;
+        const bool eq = valid && k == T;
+        if (!rank_eq) return gt || eq;
+        const uint64_t m = __ballot(eq);
+        const uint32_t r = eqr + __popcll(m & lanes_below());
+        eqr += __popcll(m);
+        return gt || (eq && r < (uint32_t)th.need);
+    };
+    uint32_t cev = 0, cmv = 0, eqr = eq_before;
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool valid = j < j1;
+        const bool keep = decide(j, valid, eqr);
+        cev += __popcll(__ballot(valid && !keep));
+        cmv += __popcll(__ballot(valid && keep && j >= N));
+    }
+    if (lane == 0) {
+        H.bc[32 + w] = cev;
+        H.bc[64 + w] = cmv;
     }
     __syncthreads();
-    return (int)mv_off;
+    uint32_t ev_off = 0, mv_off = 0, mv_tot = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const uint32_t e = H.bc[32 + i], m = H.bc[64 + i];
+        ev_off += i < w ? e : 0u;
+        mv_off += i < w ? m : 0u;
+        mv_tot += m;
+    }
+    eqr = eq_before;
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool valid = j < j1;
+        const bool keep = decide(j, valid, eqr);
+        const bool ev = valid && !keep;
+        const bool mv = valid && keep && j >= N;
+        const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
+        const uint32_t rev = ev_off + __popcll(mev & lanes_below());
+        const uint32_t rmv = mv_off + __popcll(mmv & lanes_below());
+        if (ev && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
+        if (mv && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
+        if (keep_out && valid) keep_out[j] = keep ? 1 : 0;
+        ev_off += __popcll(mev);
+        mv_off += __popcll(mmv);
+    }
+    __syncthreads();
+    return (int)mv_tot;
 }
 
 // ---------------------------------------------------------------- the pass
@@ -340,7 +435,6 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         return;
     }
 
-    // ---- mean: sum the rows not yet summed (Sec. 3.2, Eq. vd) ----
     int count = 0;
     if (st) {
         const double c = st[D];
@@ -354,6 +448,14 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     auto sfetch = [&](int r, int c) -> uint4 {
         return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
     };
+    auto ident = [](int e) { return e; };
+
+    // the first two tiles of the old rows go out now; they land while the mean is formed
+    uint4 pre_a[kUnroll], pre_b[kUnroll];
+    const bool score_old = need_scores && count > 0;
+    if (score_old) load_first2<DT, D>(count, ident, gfetch, pre_a, pre_b);
+
+    // ---- mean: sum the rows not yet summed (Sec. 3.2, Eq. vd) ----
     {
         double acc[S::EPL];
 #pragma unroll
@@ -362,10 +464,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                         [&](int e, bool valid, uint4 w) {
                             float x[S::EPL];
                             E::unpack(w, x);
+                            if (valid) {
 #pragma unroll
-                            for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
-                            if (stashed && valid)
-                                *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
+                                for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+                                if (stashed)
+                                    *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
+                            }
                         });
         block_col_sums<DT, D>(acc, red, H.sum);
     }
@@ -396,6 +500,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // ---- scores (Sec. 3.2) ----
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
     uint64_t best = ~0ull;                    // (key << 32) | ~slot: min = lowest score, highest slot
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
     if (need_scores) {
         float m[S::EPL];
 #pragma unroll
@@ -436,7 +541,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             }
             if (cl == 0 && valid) {
                 const uint32_t key = orderable(s);
-                if (to_lds) keys[r] = key;
+                if (to_lds) {
+                    keys[r] = key;
+                    kmin = min(kmin, key);
+                    kmax = max(kmax, key);
+                }
                 if (amode) {
                     const uint64_t c = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
                     best = c < best ? c : best;
@@ -444,14 +553,13 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 if (scores_out) scores_out[r] = s;
             }
         };
-        for_rows<DT, D>(count, [](int e) { return e; }, gfetch,
-                        [&](int e, bool valid, uint4 w) { on_row(e, valid, w); });
+        if (score_old) for_rows_pre2<DT, D>(count, ident, gfetch, on_row, pre_a, pre_b);
+        auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
+        auto fresh_row = [&](int e) { return count + e; };
         if (stashed)
-            for_rows<DT, D>(fresh, [&](int e) { return count + e; }, sfetch,
-                            [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); });
+            for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
         else
-            for_rows<DT, D>(fresh, [&](int e) { return count + e; }, gfetch,
-                            [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); });
+            for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
     }
     __syncthreads();
     if (score_mode) return;
@@ -482,58 +590,68 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = j == victim ? 0 : 1;
             __syncthreads();
         } else {
-            const Threshold th = radix_select(keys, n, N, H);
+            const Threshold th = select_threshold(keys, n, N, kmin, kmax, H);
             n_moves = build_lists(keys, n, N, th, evl, p.evict_cap, mvl, p.move_cap, keep_out, H);
         }
     } else {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
     }
 
-    // ---- running sum: remove the evicted rows ----
-    if (st) {
-        if (evict) {
-            double acc[S::EPL];
-#pragma unroll
-            for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
-            auto body = [&](int, bool, uint4 w) {
-                float x[S::EPL];
-                E::unpack(w, x);
-#pragma unroll
-                for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
-            };
-            auto fetch = [&](int r, int c) -> uint4 {
-                return (stashed && r >= count) ? sfetch(r, c) : gfetch(r, c);
-            };
-            for_rows<DT, D>(n - N, [&](int e) { return (int)evl[e]; }, fetch, body);
-            // red aliases keys, which the lists no longer need
-            block_col_sums<DT, D>(acc, red, H.sum_ev);
-            for (int t = threadIdx.x; t < D; t += NT) st[t] = H.sum[t] - H.sum_ev[t];
-            if (threadIdx.x == 0) st[D] = (double)N;
-        } else {
-            for (int t = threadIdx.x; t < D; t += NT) st[t] = H.sum[t];
-            if (threadIdx.x == 0) st[D] = (double)n;
-        }
-        __syncthreads();
-    }
-
-    // ---- gather with slot reuse ----
-    if (n_moves > 0) {
+    // ---- gather with slot reuse, and the evicted rows leave the running sum ----
+    if (evict) {
+        const int n_ev = n - N;  // evl[0, n_moves) are the holes, the rest lie at or above N
         char *kb = p.k ? p.k + off : nullptr;
         char *vw = p.v + off;
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
-        const int lane_q = lane / S::LPR;
-        const int g = wave_id() * S::RPW + lane_q;  // row group of this lane
-        for (int e = g; e < n_moves; e += S::GROUPS) {
-            const int dst = (int)evl[e];
-            const int src = (int)mvl[e];
-            if (kb) {
-                const uint4 kv = *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16);
-                *reinterpret_cast<uint4 *>(kb + (int64_t)dst * ss + cl * 16) = kv;
+        const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
+        auto vfetch = [&](int r) -> uint4 {
+            return (stashed && r >= count) ? sfetch(r, cl) : gfetch(r, cl);
+        };
+        double acc[S::EPL];
+#pragma unroll
+        for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
+        const int todo = st ? n_ev : n_moves;
+        for (int e0 = 0; e0 < todo; e0 += S::STEP) {
+            uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int e = e0 + k * S::GROUPS + g;
+                const int ec = e < todo ? e : todo - 1;
+                if (st) vh[k] = vfetch((int)evl[ec]);
+                if (ec < n_moves) {
+                    const int src = (int)mvl[ec];
+                    km[k] = kb ? *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16)
+                               : make_uint4(0u, 0u, 0u, 0u);
+                    vm[k] = vfetch(src);
+                }
             }
-            const uint4 vv = (stashed && src >= count) ? sfetch(src, cl) : gfetch(src, cl);
-            *reinterpret_cast<uint4 *>(vw + (int64_t)dst * ss + cl * 16) = vv;
-            if (pos && cl == 0) pos[dst] = pos[src];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int e = e0 + k * S::GROUPS + g;
+                if (e >= todo) continue;
+                if (st) {
+                    float x[S::EPL];
+                    E::unpack(vh[k], x);
+#pragma unroll
+                    for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+                }
+                if (e < n_moves) {
+                    const int dst = (int)evl[e];
+                    const int src = (int)mvl[e];
+                    if (kb) *reinterpret_cast<uint4 *>(kb + (int64_t)dst * ss + cl * 16) = km[k];
+                    *reinterpret_cast<uint4 *>(vw + (int64_t)dst * ss + cl * 16) = vm[k];
+                    if (pos && cl == 0) pos[dst] = pos[src];
+                }
+            }
         }
+        if (st) {
+            block_col_sums<DT, D>(acc, red, H.sum_ev);  // red aliases keys, no longer needed
+            for (int t = threadIdx.x; t < D; t += NT) st[t] = H.sum[t] - H.sum_ev[t];
+            if (threadIdx.x == 0) st[D] = (double)N;
+        }
+    } else if (st) {
+        for (int t = threadIdx.x; t < D; t += NT) st[t] = H.sum[t];
+        if (threadIdx.x == 0) st[D] = (double)n;
     }
 }
 
@@ -553,26 +671,16 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
         for (int j = threadIdx.x; j < n; j += NT) keep[j] = 1;
         return;
     }
-    for (int j = threadIdx.x; j < n; j += NT) keys[j] = orderable(sc[j]);
-    __syncthreads();
-    const Threshold th = radix_select(keys, n, N, H);
-    const bool rank_eq = th.count_eq != th.need;
-    uint32_t eq_off = 0;
-    for (int base = 0; base < n; base += NT) {
-        const int j = base + threadIdx.x;
-        const bool valid = j < n;
-        const uint32_t k = valid ? keys[j] : 0u;
-        const bool gt = valid && k > th.key;
-        const bool eq = valid && k == th.key;
-        bool kp = gt || eq;
-        if (rank_eq) {
-            uint32_t tot;
-            const uint32_t r = block_rank(eq, H.bc, tot) + eq_off;
-            eq_off += tot;
-            kp = gt || (eq && r < (uint32_t)th.need);
-        }
-        if (valid) keep[j] = kp ? 1 : 0;
+    uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
+    for (int j = threadIdx.x; j < n; j += NT) {
+        const uint32_t k = orderable(sc[j]);
+        keys[j] = k;
+        kmin = min(kmin, k);
+        kmax = max(kmax, k);
     }
+    __syncthreads();
+    const Threshold th = select_threshold(keys, n, N, kmin, kmax, H);
+    build_lists(keys, n, N, th, nullptr, 0, nullptr, 0, keep, H);
 }
 
 // Standalone gather from a keep mask.
@@ -592,28 +700,51 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     if (n <= N) return;
     const int64_t cap = p.capacity;
     const uint8_t *keep = p.keep_in + u * cap;
-    uint32_t h_off = 0, m_off = 0;
-    for (int base = 0; base < n; base += NT) {
-        const int j = base + threadIdx.x;
-        const bool valid = j < n;
-        const bool kp = valid && keep[j] != 0;
-        uint32_t th, tm;
-        const uint32_t rh = block_rank(valid && j < N && !kp, H.bc, th) + h_off;
-        const uint32_t rm = block_rank(kp && j >= N, H.bc, tm) + m_off;
-        if (valid && j < N && !kp && rh < (uint32_t)p.evict_cap) holes[rh] = (uint32_t)j;
-        if (kp && j >= N && rm < (uint32_t)p.move_cap) movers[rm] = (uint32_t)j;
-        h_off += th;
-        m_off += tm;
+    // wave-segmented ranks of holes (slots < N, not kept) and movers (slots >= N, kept)
+    const int w = wave_id(), lane = lane_id();
+    const int seg = (((n + NW - 1) / NW) + 63) & ~63;
+    const int j0 = w * seg, j1 = min(n, j0 + seg);
+    uint32_t ch = 0, cm = 0;
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool kp = j < j1 && keep[j] != 0;
+        ch += __popcll(__ballot(j < j1 && j < N && !kp));
+        cm += __popcll(__ballot(kp && j >= N));
+    }
+    if (lane == 0) {
+        H.bc[w] = ch;
+        H.bc[32 + w] = cm;
     }
     __syncthreads();
-    int moves = (int)min(h_off, m_off);
+    uint32_t h_off = 0, m_off = 0, h_tot = 0, m_tot = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        h_off += i < w ? H.bc[i] : 0u;
+        m_off += i < w ? H.bc[32 + i] : 0u;
+        h_tot += H.bc[i];
+        m_tot += H.bc[32 + i];
+    }
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool kp = j < j1 && keep[j] != 0;
+        const bool hole = j < j1 && j < N && !kp;
+        const bool mover = kp && j >= N;
+        const uint64_t mh = __ballot(hole), mm = __ballot(mover);
+        const uint32_t rh = h_off + __popcll(mh & lanes_below());
+        const uint32_t rm = m_off + __popcll(mm & lanes_below());
+        if (hole && rh < (uint32_t)p.evict_cap) holes[rh] = (uint32_t)j;
+        if (mover && rm < (uint32_t)p.move_cap) movers[rm] = (uint32_t)j;
+        h_off += __popcll(mh);
+        m_off += __popcll(mm);
+    }
+    __syncthreads();
+    int moves = (int)min(h_tot, m_tot);
     moves = min(moves, min(p.evict_cap, p.move_cap));
     const int64_t off = (int64_t)sl * p.s_seq + (int64_t)layer * p.s_layer + (int64_t)head * p.s_head;
     char *kb = p.k ? p.k + off : nullptr;
     char *vb = p.v + off;
     int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
     const int64_t ss = p.s_slot;
-    const int lane = lane_id();
     const int cl = lane % S::LPR;
     const int g = wave_id() * S::RPW + lane / S::LPR;
     for (int e = g; e < moves; e += S::GROUPS) {

@@ -15,9 +15,14 @@ constexpr int kLdsBytes = 160 * 1024;     // LDS of one gfx950 workgroup
 enum Mode : int32_t { kModeStep = 0, kModeScore = 1 };
 
 // Fixed head of the dynamic LDS of every kernel.
+constexpr int kBins = 1024;                // histogram bins of the selection
+constexpr int kCand = 64;                  // candidates ranked directly by one wave
+
 struct LdsHead {
     uint32_t bc[128];     // broadcast slots and per-wave partials
-    uint32_t hist[256];   // radix histogram
+    uint32_t hist[kBins]; // selection histogram
+    uint32_t cand_key[kCand];
+    uint32_t cand_idx[kCand];
     float mean[256];      // fp32 mean used for scoring
     float udir[256];      // mean / ||mean|| (direction variant)
     double sum[256];      // fp64 column sums
