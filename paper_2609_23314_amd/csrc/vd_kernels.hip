@@ -65,7 +65,7 @@ template <int DT, int D> struct Shape {
     static constexpr int RPW = 64 / LPR;              // rows per wave instruction
     static constexpr int GROUPS = NW * RPW;           // row groups per workgroup
     static constexpr int STEP = GROUPS * kUnroll;     // rows per tile
-    static_assert(LPR >= 1 && LPR <= 64 && 64 % LPR == 0, "unsupported row shape");
+    static_assert(LPR >= 8 && LPR <= 64 && 64 % LPR == 0, "unsupported row shape");
 };
 
 // ---------------------------------------------------------------- lane utils
@@ -90,12 +90,41 @@ template <int LPR> __device__ __forceinline__ float row_sum(float x) {
     return x;
 }
 
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xF, false);
+}
+__device__ __forceinline__ uint32_t lane_u32(uint32_t x, int lane) {
+    return (uint32_t)__builtin_amdgcn_readlane((int)x, lane);
+}
+
+// Wave-wide minimum / maximum: DPP inside each 16-lane row, then the four
+// row results by readlane.
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
-    for (int o = 32; o > 0; o >>= 1) x = min(x, (uint32_t)__shfl_xor((int)x, o));
-    return x;
+    x = min(x, dpp_u32<0xB1>(x));
+    x = min(x, dpp_u32<0x4E>(x));
+    x = min(x, dpp_u32<0x141>(x));
+    x = min(x, dpp_u32<0x140>(x));
+    return min(min(lane_u32(x, 0), lane_u32(x, 16)), min(lane_u32(x, 32), lane_u32(x, 48)));
 }
 __device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) {
-    for (int o = 32; o > 0; o >>= 1) x = max(x, (uint32_t)__shfl_xor((int)x, o));
+    x = max(x, dpp_u32<0xB1>(x));
+    x = max(x, dpp_u32<0x4E>(x));
+    x = max(x, dpp_u32<0x141>(x));
+    x = max(x, dpp_u32<0x140>(x));
+    return max(max(lane_u32(x, 0), lane_u32(x, 16)), max(lane_u32(x, 32), lane_u32(x, 48)));
+}
+
+// Inclusive prefix sum over the wave's lanes: shifts of 1, 2, 4, 8 inside
+// each row (row_shr, zero fill), then rows 1 and 3 add lane 15 of the row
+// before (row_bcast:15) and rows 2 and 3 add lane 31 (row_bcast:31).
+__device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
+    x += dpp_u32<0x111>(x);
+    x += dpp_u32<0x112>(x);
+    x += dpp_u32<0x114>(x);
+    x += dpp_u32<0x118>(x);
+    x += dpp_u32<0x142, 0xA>(x);
+    x += dpp_u32<0x143, 0xC>(x);
     return x;
 }
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
@@ -104,6 +133,21 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
         x = y < x ? y : x;
     }
     return x;
+}
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load that bypasses cache retention: the value rows stream through once.
+__device__ __forceinline__ uint4 load_stream(const char *p) {
+    const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(t.x, t.y, t.z, t.w);
+}
+
+// 16-byte store that is not kept in the cache: moved rows are not read again here.
+__device__ __forceinline__ void store_stream(char *p, uint4 v) {
+    u32x4 t;
+    t.x = v.x; t.y = v.y; t.z = v.z; t.w = v.w;
+    __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
 }
 
 // Order-preserving map of an fp32 value onto uint32 (-0 taken as +0).
@@ -149,24 +193,26 @@ template <int DT, int D, typename RowOf, typename Fetch, typename Body>
 __device__ __forceinline__ void for_rows_pre2(int count, RowOf row_of, Fetch fetch, Body body,
                                               uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
     using S = Shape<DT, D>;
+    // Loads are issued unconditionally (past the end they re-read the last row),
+    // so every iteration leaves the same two tiles in flight and the in-order
+    // load counter lets each use wait for exactly its own tile.
     const int ntiles = (count + S::STEP - 1) / S::STEP;
     int t = 0;
     for (; t + 1 < ntiles; t += 2) {
         use_tile<DT, D>(t, count, a, body);
-        if (t + 2 < ntiles) load_tile<DT, D>(t + 2, count, row_of, fetch, a);
+        load_tile<DT, D>(t + 2, count, row_of, fetch, a);
         use_tile<DT, D>(t + 1, count, b, body);
-        if (t + 3 < ntiles) load_tile<DT, D>(t + 3, count, row_of, fetch, b);
+        load_tile<DT, D>(t + 3, count, row_of, fetch, b);
     }
     if (t < ntiles) use_tile<DT, D>(t, count, a, body);
 }
 
-// Loads the first two tiles of a stream (the second only if it exists).
+// Loads the first two tiles of a stream (clamped like every other tile).
 template <int DT, int D, typename RowOf, typename Fetch>
 __device__ __forceinline__ void load_first2(int count, RowOf row_of, Fetch fetch,
                                             uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
-    using S = Shape<DT, D>;
     load_tile<DT, D>(0, count, row_of, fetch, a);
-    if (count > S::STEP) load_tile<DT, D>(1, count, row_of, fetch, b);
+    load_tile<DT, D>(1, count, row_of, fetch, b);
 }
 
 template <int DT, int D, typename RowOf, typename Fetch, typename Body>
@@ -177,15 +223,40 @@ __device__ __forceinline__ void for_rows(int count, RowOf row_of, Fetch fetch, B
     for_rows_pre2<DT, D>(count, row_of, fetch, body, a, b);
 }
 
+// x + (x of lane ^ 8, 16 or 32): each lane pair ends with the same bits.
+template <int O> __device__ __forceinline__ double xor_sum(double x) {
+    const unsigned long long b = __double_as_longlong(x);
+    const unsigned lo = (unsigned)b, hi = (unsigned)(b >> 32);
+    if constexpr (O == 8) {  // row_ror:8 swaps the two halves of each 16-lane row
+        const unsigned rlo = (unsigned)__builtin_amdgcn_update_dpp(0, (int)lo, 0x128, 0xF, 0xF, false);
+        const unsigned rhi = (unsigned)__builtin_amdgcn_update_dpp(0, (int)hi, 0x128, 0xF, 0xF, false);
+        return x + __longlong_as_double(((unsigned long long)rhi << 32) | rlo);
+    } else {
+        // permlane swaps pair rows (16) or wave halves (32); both outputs hold
+        // the lower lane's value first, so the sum is the same on both lanes
+        const auto L = O == 16 ? __builtin_amdgcn_permlane16_swap(lo, lo, false, false)
+                               : __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+        const auto Hi = O == 16 ? __builtin_amdgcn_permlane16_swap(hi, hi, false, false)
+                                : __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+        const double a = __longlong_as_double(((unsigned long long)Hi[0] << 32) | L[0]);
+        const double c = __longlong_as_double(((unsigned long long)Hi[1] << 32) | L[1]);
+        return a + c;
+    }
+}
+
 // Column sums of per-lane fp64 partials (each lane holds EPL columns of its
-// chunk) into out[0..D) in LDS; fixed reduction order.  `red` holds NW*D doubles.
+// chunk) into out[0..D) in LDS; fixed reduction order.  `red` holds NW*D
+// doubles; `out` may be red itself (each thread reads and then writes only
+// its own column).
 template <int DT, int D>
 __device__ __forceinline__ void block_col_sums(double *acc, double *red, double *out) {
     using S = Shape<DT, D>;
 #pragma unroll
-    for (int o = S::LPR; o < 64; o <<= 1)
-#pragma unroll
-        for (int i = 0; i < S::EPL; ++i) acc[i] += __shfl_xor(acc[i], o);
+    for (int i = 0; i < S::EPL; ++i) {
+        if constexpr (S::LPR <= 8) acc[i] = xor_sum<8>(acc[i]);
+        if constexpr (S::LPR <= 16) acc[i] = xor_sum<16>(acc[i]);
+        if constexpr (S::LPR <= 32) acc[i] = xor_sum<32>(acc[i]);
+    }
     const int lane = lane_id(), w = wave_id();
     if (lane < S::LPR)
 #pragma unroll
@@ -245,20 +316,18 @@ __device__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32
             if (k >= lo && k <= hi) atomicAdd(&H.hist[(k - lo) >> shift], 1u);
         }
         __syncthreads();
-        // suffix sums over the bins: thread t owns bin t
-        const uint32_t h = H.hist[threadIdx.x];
-        uint32_t suf = h;
-        for (int o = 1; o < 64; o <<= 1) {
-            const uint32_t v = __shfl_down(suf, o);
-            if (lane_id() + o < 64) suf += v;
-        }
-        if (lane_id() == 0) H.bc[wave_id()] = suf;  // wave totals
+        // thread t owns bin kBins-1-t, so a prefix sum in thread order counts
+        // the keys in higher bins
+        const uint32_t bin = kBins - 1 - threadIdx.x;
+        const uint32_t h = H.hist[bin];
+        const uint32_t incl = wave_incl_scan(h);
+        if (lane_id() == 63) H.bc[wave_id()] = incl;  // wave totals
         __syncthreads();
-        uint32_t above = suf - h;
-        for (int i = wave_id() + 1; i < NW; ++i) above += H.bc[i];
+        uint32_t above = incl - h;
+        for (int i = 0; i < wave_id(); ++i) above += H.bc[i];
         const uint32_t un = (uint32_t)need;
         if (above < un && un <= above + h) {
-            H.bc[64] = threadIdx.x;
+            H.bc[64] = bin;
             H.bc[65] = above;
             H.bc[66] = h;
         }
@@ -283,28 +352,27 @@ __device__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32
             }
         }
         __syncthreads();
-        if (wave_id() == 0) {
+        {
+            // lane t holds candidate t; wave w ranks candidates w, w+16, w+32, w+48
+            // by counting, with one ballot, the candidates that order before each
             const int c = in_range;
-            const int i = lane_id();
-            const uint32_t ki = i < c ? H.cand_key[i] : 0u;
-            const uint32_t ji = i < c ? H.cand_idx[i] : 0u;
-            int rank = 0;
-            for (int t = 0; t < c; ++t) {  // t is wave-uniform: operands come by readlane
-                const uint32_t kt = (uint32_t)__builtin_amdgcn_readlane((int)ki, t);
-                const uint32_t jt = (uint32_t)__builtin_amdgcn_readlane((int)ji, t);
-                rank += (kt > ki || (kt == ki && jt < ji)) ? 1 : 0;
-            }
-            if (i >= c) rank = -1;
-            // the candidate ranked need-1 fixes the threshold key
-            const uint64_t m = __ballot(rank == need - 1);
-            const int src = __ffsll((unsigned long long)m) - 1;
-            const uint32_t T = __shfl(ki, src);
-            const uint32_t n_gt = __popcll(__ballot(i < c && ki > T));
-            const uint32_t n_eq = __popcll(__ballot(i < c && ki == T));
-            if (i == 0) {
-                H.bc[67] = T;
-                H.bc[68] = (uint32_t)need - n_gt;
-                H.bc[69] = n_eq;
+            const int t = lane_id();
+            const bool live = t < c;
+            const uint32_t kt = live ? H.cand_key[t] : 0u;
+            const uint32_t jt = live ? H.cand_idx[t] : 0u;
+            for (int i = wave_id(); i < c; i += NW) {
+                const uint32_t ki = lane_u32(kt, i), ji = lane_u32(jt, i);
+                const uint32_t rank =
+                    __popcll(__ballot(live && (kt > ki || (kt == ki && jt < ji))));
+                if (rank == (uint32_t)(need - 1)) {  // the candidate that fixes the threshold
+                    const uint32_t n_gt = __popcll(__ballot(live && kt > ki));
+                    const uint32_t n_eq = __popcll(__ballot(live && kt == ki));
+                    if (t == 0) {
+                        H.bc[67] = ki;
+                        H.bc[68] = (uint32_t)need - n_gt;
+                        H.bc[69] = n_eq;
+                    }
+                }
             }
         }
         __syncthreads();
@@ -442,124 +510,147 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     }
     const int fresh = n - count;
     const bool stashed = fresh <= p.stash_rows;
-    auto gfetch = [&](int r, int c) -> uint4 {
-        return *reinterpret_cast<const uint4 *>(vb + (int64_t)r * ss + c * 16);
-    };
+    auto gfetch = [&](int r, int c) -> uint4 { return load_stream(vb + (int64_t)r * ss + c * 16); };
     auto sfetch = [&](int r, int c) -> uint4 {
         return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
     };
-    auto ident = [](int e) { return e; };
-
-    // the first two tiles of the old rows go out now; they land while the mean is formed
-    uint4 pre_a[kUnroll], pre_b[kUnroll];
+    const int lastrow = n - 1;
+    auto fresh_row = [&](int e) { return min(count + e, lastrow); };
+    auto old_row = [&](int e) { return min(e, lastrow); };
     const bool score_old = need_scores && count > 0;
-    if (score_old) load_first2<DT, D>(count, ident, gfetch, pre_a, pre_b);
-
-    // ---- mean: sum the rows not yet summed (Sec. 3.2, Eq. vd) ----
-    {
-        double acc[S::EPL];
-#pragma unroll
-        for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
-        for_rows<DT, D>(fresh, [&](int e) { return count + e; }, gfetch,
-                        [&](int e, bool valid, uint4 w) {
-                            float x[S::EPL];
-                            E::unpack(w, x);
-                            if (valid) {
-#pragma unroll
-                                for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
-                                if (stashed)
-                                    *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
-                            }
-                        });
-        block_col_sums<DT, D>(acc, red, H.sum);
-    }
-    for (int t = threadIdx.x; t < D; t += NT) {
-        const double s = (count > 0 ? st[t] : 0.0) + H.sum[t];
-        H.sum[t] = s;
-        H.mean[t] = (float)(s / (double)n);
-    }
-    __syncthreads();
-    bool mean_zero = false;
-    if constexpr (VAR == 1) {
-        if (wave_id() == 0) {
-            float a = 0.f;
-            for (int t = lane; t < D; t += 64) a += H.mean[t] * H.mean[t];
-            for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o);
-            if (lane == 0) H.bc[0] = __float_as_uint(a);
-        }
-        __syncthreads();
-        const float mn2 = __uint_as_float(H.bc[0]);
-        const float mn = sqrtf(mn2);
-        mean_zero = !(mn2 > 0.f);
-        for (int t = threadIdx.x; t < D; t += NT) H.udir[t] = mean_zero ? 0.f : H.mean[t] / mn;
-        __syncthreads();
-    }
-    if (score_mode && p.mean_out)
-        for (int t = threadIdx.x; t < D; t += NT) p.mean_out[u * D + t] = H.mean[t];
-
-    // ---- scores (Sec. 3.2) ----
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
+    if (evict && p.k && threadIdx.x == 0) {
+        // one early read of the unit's K slab warms its address translation
+        // before the gather moves K rows; the value itself is not needed
+        const uint32_t probe = __builtin_nontemporal_load(
+            reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss));
+        if (probe == 0x7FC00001u) H.bc[127] = probe;  // keeps the load; nothing reads bc[127]
+    }
+    const bool to_lds = evict && !amode;
     uint64_t best = ~0ull;                    // (key << 32) | ~slot: min = lowest score, highest slot
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
-    if (need_scores) {
-        float m[S::EPL];
+    float m[S::EPL];                          // this lane's columns of v_bar (Dir: v_bar / |v_bar|)
+    bool mean_zero = false;
+
+    // ---- mean: sum the rows not yet summed (Sec. 3.2, Eq. vd) ----
+    double acc[S::EPL];
+#pragma unroll
+    for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
+    auto mean_body = [&](int e, bool valid, uint4 w) {
+        float x[S::EPL];
+        E::unpack(w, x);
+        if (valid) {
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+            if (stashed) *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
+        }
+    };
+    auto finish_mean = [&]() {
+        block_col_sums<DT, D>(acc, red, H.sum);
+        for (int t = threadIdx.x; t < D; t += NT) {
+            const double old_sum = count > 0 ? st[t] : 0.0;
+            const double s = old_sum + H.sum[t];
+            H.old_sum[t] = old_sum;
+            H.sum[t] = s;
+            H.mean[t] = (float)(s / (double)n);
+        }
+        __syncthreads();
+        if constexpr (VAR == 1) {
+            if (wave_id() == 0) {
+                float a = 0.f;
+                for (int t = lane; t < D; t += 64) a += H.mean[t] * H.mean[t];
+                for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o);
+                if (lane == 0) H.bc[0] = __float_as_uint(a);
+            }
+            __syncthreads();
+            const float mn2 = __uint_as_float(H.bc[0]);
+            const float mn = sqrtf(mn2);
+            mean_zero = !(mn2 > 0.f);
+            for (int t = threadIdx.x; t < D; t += NT) H.udir[t] = mean_zero ? 0.f : H.mean[t] / mn;
+            __syncthreads();
+        }
+        if (score_mode && p.mean_out)
+            for (int t = threadIdx.x; t < D; t += NT) p.mean_out[u * D + t] = H.mean[t];
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) m[i] = (VAR == 1 ? H.udir : H.mean)[cl * S::EPL + i];
-        const bool to_lds = evict && !amode;
-        auto on_row = [&](int r, bool valid, uint4 w) {
-            float x[S::EPL];
-            E::unpack(w, x);
-            float s;
-            if constexpr (VAR == 0) {  // L2: ||v - v_bar||
-                float a = 0.f;
+    };
+
+    // ---- scores (Sec. 3.2) ----
+    auto on_row = [&](int r, bool valid, uint4 w) {
+        float x[S::EPL];
+        E::unpack(w, x);
+        float s;
+        if constexpr (VAR == 0) {  // L2: ||v - v_bar||
+            float a = 0.f;
 #pragma unroll
-                for (int i = 0; i < S::EPL; ++i) {
-                    const float t = x[i] - m[i];
-                    a = fmaf(t, t, a);
-                }
-                s = sqrtf(row_sum<S::LPR>(a));
-            } else if constexpr (VAR == 2) {  // Norm: ||v||
-                float a = 0.f;
-#pragma unroll
-                for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
-                s = sqrtf(row_sum<S::LPR>(a));
-            } else {  // Dir: 1 - cos = ||v/|v| - v_bar/|v_bar| ||^2 / 2
-                float a = 0.f;
-#pragma unroll
-                for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
-                const float nv2 = row_sum<S::LPR>(a);
-                const bool ok = nv2 > 0.f && !mean_zero;
-                const float inv = ok ? 1.0f / sqrtf(nv2) : 0.f;
-                float b = 0.f;
-#pragma unroll
-                for (int i = 0; i < S::EPL; ++i) {
-                    const float t = fmaf(x[i], inv, -m[i]);
-                    b = fmaf(t, t, b);
-                }
-                const float half = 0.5f * row_sum<S::LPR>(b);
-                s = ok ? half : 1.0f;
+            for (int i = 0; i < S::EPL; ++i) {
+                const float t = x[i] - m[i];
+                a = fmaf(t, t, a);
             }
-            if (cl == 0 && valid) {
-                const uint32_t key = orderable(s);
-                if (to_lds) {
-                    keys[r] = key;
-                    kmin = min(kmin, key);
-                    kmax = max(kmax, key);
-                }
-                if (amode) {
-                    const uint64_t c = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
-                    best = c < best ? c : best;
-                }
-                if (scores_out) scores_out[r] = s;
+            s = sqrtf(row_sum<S::LPR>(a));
+        } else if constexpr (VAR == 2) {  // Norm: ||v||
+            float a = 0.f;
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
+            s = sqrtf(row_sum<S::LPR>(a));
+        } else {  // Dir: 1 - cos = ||v/|v| - v_bar/|v_bar| ||^2 / 2
+            float a = 0.f;
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
+            const float nv2 = row_sum<S::LPR>(a);
+            const bool ok = nv2 > 0.f && !mean_zero;
+            const float inv = ok ? 1.0f / sqrtf(nv2) : 0.f;
+            float b = 0.f;
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) {
+                const float t = fmaf(x[i], inv, -m[i]);
+                b = fmaf(t, t, b);
             }
-        };
-        if (score_old) for_rows_pre2<DT, D>(count, ident, gfetch, on_row, pre_a, pre_b);
-        auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
-        auto fresh_row = [&](int e) { return count + e; };
-        if (stashed)
-            for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
-        else
-            for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
+            const float half = 0.5f * row_sum<S::LPR>(b);
+            s = ok ? half : 1.0f;
+        }
+        if (cl == 0 && valid) {
+            const uint32_t key = orderable(s);
+            if (to_lds) {
+                keys[r] = key;
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
+            if (amode) {
+                const uint64_t c = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
+                best = c < best ? c : best;
+            }
+            if (scores_out) scores_out[r] = s;
+        }
+    };
+
+    auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
+    if (score_old && fresh <= 2 * S::STEP) {
+        // the new block fits two tiles: it is read alone (every CU's new rows
+        // then reach the memory controllers ahead of any old-row traffic), and
+        // the first two tiles of the old rows go out as soon as it has landed,
+        // to arrive while the mean is reduced
+        uint4 new_a[kUnroll], new_b[kUnroll], pre_a[kUnroll], pre_b[kUnroll];
+        const int fl = fresh > 0 ? fresh : 1;
+        load_first2<DT, D>(fl, fresh_row, gfetch, new_a, new_b);
+        use_tile<DT, D>(0, fresh, new_a, mean_body);
+        use_tile<DT, D>(1, fresh, new_b, mean_body);
+        __builtin_amdgcn_sched_barrier(0);
+        load_first2<DT, D>(count, old_row, gfetch, pre_a, pre_b);
+        __builtin_amdgcn_sched_barrier(0);
+        finish_mean();
+        // the staged new rows are scored from LDS while the old-row tiles are in flight
+        if (stashed) for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
+        for_rows_pre2<DT, D>(count, old_row, gfetch, on_row, pre_a, pre_b);
+        if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
+    } else {
+        for_rows<DT, D>(fresh, fresh_row, gfetch, mean_body);
+        finish_mean();
+        if (need_scores) {
+            if (stashed) for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
+            if (score_old) for_rows<DT, D>(count, old_row, gfetch, on_row);
+            if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
+        }
     }
     __syncthreads();
     if (score_mode) return;
@@ -598,19 +689,25 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     }
 
     // ---- gather with slot reuse, and the evicted rows leave the running sum ----
+    // In steady state (the state covered exactly the N old rows) the new sum is
+    // old - holes + movers, so only the rows that move are read; otherwise it
+    // is total - every evicted row.
     if (evict) {
         const int n_ev = n - N;  // evl[0, n_moves) are the holes, the rest lie at or above N
+        const bool steady = st && count == N;
         char *kb = p.k ? p.k + off : nullptr;
         char *vw = p.v + off;
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
         const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
         auto vfetch = [&](int r) -> uint4 {
-            return (stashed && r >= count) ? sfetch(r, cl) : gfetch(r, cl);
+            return (stashed && r >= count)
+                       ? sfetch(r, cl)
+                       : *reinterpret_cast<const uint4 *>(vb + (int64_t)r * ss + cl * 16);
         };
         double acc[S::EPL];
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
-        const int todo = st ? n_ev : n_moves;
+        const int todo = (st && !steady) ? n_ev : n_moves;
         for (int e0 = 0; e0 < todo; e0 += S::STEP) {
             uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
 #pragma unroll
@@ -633,20 +730,26 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                     float x[S::EPL];
                     E::unpack(vh[k], x);
 #pragma unroll
-                    for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+                    for (int i = 0; i < S::EPL; ++i) acc[i] -= (double)x[i];
+                    if (steady) {
+                        E::unpack(vm[k], x);
+#pragma unroll
+                        for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+                    }
                 }
                 if (e < n_moves) {
                     const int dst = (int)evl[e];
                     const int src = (int)mvl[e];
-                    if (kb) *reinterpret_cast<uint4 *>(kb + (int64_t)dst * ss + cl * 16) = km[k];
-                    *reinterpret_cast<uint4 *>(vw + (int64_t)dst * ss + cl * 16) = vm[k];
+                    if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, km[k]);
+                    store_stream(vw + (int64_t)dst * ss + cl * 16, vm[k]);
                     if (pos && cl == 0) pos[dst] = pos[src];
                 }
             }
         }
         if (st) {
-            block_col_sums<DT, D>(acc, red, H.sum_ev);  // red aliases keys, no longer needed
-            for (int t = threadIdx.x; t < D; t += NT) st[t] = H.sum[t] - H.sum_ev[t];
+            block_col_sums<DT, D>(acc, red, red);  // red aliases keys, no longer needed
+            for (int t = threadIdx.x; t < D; t += NT)
+                st[t] = (steady ? H.old_sum[t] : H.sum[t]) + red[t];
             if (threadIdx.x == 0) st[D] = (double)N;
         }
     } else if (st) {

@@ -25,8 +25,8 @@ struct LdsHead {
     uint32_t cand_idx[kCand];
     float mean[256];      // fp32 mean used for scoring
     float udir[256];      // mean / ||mean|| (direction variant)
-    double sum[256];      // fp64 column sums
-    double sum_ev[256];   // fp64 column sums of the evicted rows
+    double sum[256];      // fp64 column sums of all n rows
+    double old_sum[256];  // fp64 column sums of the rows the state covered
 };
 static_assert(sizeof(LdsHead) % 16 == 0, "LDS head must keep 16-byte alignment");
 
