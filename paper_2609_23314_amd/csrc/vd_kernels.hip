@@ -707,42 +707,89 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         double acc[S::EPL];
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
-        const int todo = (st && !steady) ? n_ev : n_moves;
-        for (int e0 = 0; e0 < todo; e0 += S::STEP) {
-            uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
+        if (!st || steady) {
+            // Only the moved rows are touched.  All list reads come first, then
+            // every row load is issued unconditionally (indices clamped into the
+            // list), then the stores: no load waits behind another.
+            const char *ksrc = kb ? kb : vb;  // without K a V row stands in, unused
+            for (int e0 = 0; e0 < n_moves; e0 += S::STEP) {
+                int dst[kUnroll], src[kUnroll];
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
-                const int e = e0 + k * S::GROUPS + g;
-                const int ec = e < todo ? e : todo - 1;
-                if (st) vh[k] = vfetch((int)evl[ec]);
-                if (ec < n_moves) {
-                    const int src = (int)mvl[ec];
-                    km[k] = kb ? *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16)
-                               : make_uint4(0u, 0u, 0u, 0u);
-                    vm[k] = vfetch(src);
+                for (int k = 0; k < kUnroll; ++k) {
+                    const int e = e0 + k * S::GROUPS + g;
+                    const int ec = e < n_moves ? e : n_moves - 1;
+                    dst[k] = (int)evl[ec];
+                    src[k] = (int)mvl[ec];
+                }
+                uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
+                int32_t ps[kUnroll];
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k)
+                    km[k] = *reinterpret_cast<const uint4 *>(ksrc + (int64_t)src[k] * ss + cl * 16);
+                if (st) {
+#pragma unroll
+                    for (int k = 0; k < kUnroll; ++k)
+                        vh[k] = *reinterpret_cast<const uint4 *>(vb + (int64_t)dst[k] * ss + cl * 16);
+                }
+                if (pos) {
+#pragma unroll
+                    for (int k = 0; k < kUnroll; ++k) ps[k] = pos[src[k]];
+                }
+                if (stashed) {
+#pragma unroll
+                    for (int k = 0; k < kUnroll; ++k) vm[k] = sfetch(src[k], cl);
+                } else {
+#pragma unroll
+                    for (int k = 0; k < kUnroll; ++k)
+                        vm[k] = *reinterpret_cast<const uint4 *>(vb + (int64_t)src[k] * ss + cl * 16);
+                }
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k) {
+                    const int e = e0 + k * S::GROUPS + g;
+                    if (e >= n_moves) continue;
+                    if (st) {  // new sum = old - holes + movers
+                        float x[S::EPL], y[S::EPL];
+                        E::unpack(vh[k], x);
+                        E::unpack(vm[k], y);
+#pragma unroll
+                        for (int i = 0; i < S::EPL; ++i) acc[i] += (double)y[i] - (double)x[i];
+                    }
+                    if (kb) store_stream(kb + (int64_t)dst[k] * ss + cl * 16, km[k]);
+                    store_stream(vw + (int64_t)dst[k] * ss + cl * 16, vm[k]);
+                    if (pos && cl == 0) pos[dst[k]] = ps[k];
                 }
             }
+        } else {
+            // the state did not cover exactly the N old rows: remove every evicted row
+            for (int e0 = 0; e0 < n_ev; e0 += S::STEP) {
+                uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
-                const int e = e0 + k * S::GROUPS + g;
-                if (e >= todo) continue;
-                if (st) {
+                for (int k = 0; k < kUnroll; ++k) {
+                    const int e = e0 + k * S::GROUPS + g;
+                    const int ec = e < n_ev ? e : n_ev - 1;
+                    vh[k] = vfetch((int)evl[ec]);
+                    if (ec < n_moves) {
+                        const int src = (int)mvl[ec];
+                        km[k] = kb ? *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16)
+                                   : make_uint4(0u, 0u, 0u, 0u);
+                        vm[k] = vfetch(src);
+                    }
+                }
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k) {
+                    const int e = e0 + k * S::GROUPS + g;
+                    if (e >= n_ev) continue;
                     float x[S::EPL];
                     E::unpack(vh[k], x);
 #pragma unroll
                     for (int i = 0; i < S::EPL; ++i) acc[i] -= (double)x[i];
-                    if (steady) {
-                        E::unpack(vm[k], x);
-#pragma unroll
-                        for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
+                    if (e < n_moves) {
+                        const int dst = (int)evl[e];
+                        const int src = (int)mvl[e];
+                        if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, km[k]);
+                        store_stream(vw + (int64_t)dst * ss + cl * 16, vm[k]);
+                        if (pos && cl == 0) pos[dst] = pos[src];
                     }
-                }
-                if (e < n_moves) {
-                    const int dst = (int)evl[e];
-                    const int src = (int)mvl[e];
-                    if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, km[k]);
-                    store_stream(vw + (int64_t)dst * ss + cl * 16, vm[k]);
-                    if (pos && cl == 0) pos[dst] = pos[src];
                 }
             }
         }
