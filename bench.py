@@ -106,9 +106,11 @@ def scanned_bytes(w, n) -> int:
 # ---------------------------------------------------------------- timing
 
 def time_pool(w, states, steps, warmup, dev):
-    """Times `steps` passes, each on a fresh copy of a pre-pass state.  Returns
-    (total seconds of the timed passes, per-launch ms, per-launch algorithmic
-    and scanned bytes)."""
+    """Times `steps` passes, each on a fresh copy of a pre-pass state.  The
+    copies are made before each timed segment; inside a segment the passes run
+    back to back on one stream, bracketed by two HIP events.  Returns (wall
+    seconds of the timed segments, GPU milliseconds of the timed segments,
+    per-launch algorithmic and scanned bytes)."""
     pool_n = min(len(states), max(steps, 1))
     work = [(st[0].clone(), st[1].clone(), st[2].clone()) for st in states[:pool_n]]
 
@@ -127,28 +129,29 @@ def time_pool(w, states, steps, warmup, dev):
         st = states[i % len(states)]
         vd.vd_evict_step(work[0][0], work[0][1], st[3], w.budget, "l2", running_sum=work[0][2])
     torch.cuda.synchronize()
-    total_s, per_launch, alg, scan = 0.0, [], [], []
+    wall_s, gpu_ms, alg, scan = 0.0, 0.0, [], []
     while done < steps:
         seg = min(pool_n, steps - done)
         refill(done, seg)
         torch.cuda.synchronize()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(seg + 1)]
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
-        ev[0].record(stream)
+        e0.record(stream)
         for j in range(seg):
             st = states[(done + j) % len(states)]
             vd.vd_evict_step(work[j][0], work[j][1], st[3], w.budget, "l2",
                              running_sum=work[j][2])
-            ev[j + 1].record(stream)
+        e1.record(stream)
         torch.cuda.synchronize()
-        total_s += time.perf_counter() - t0
+        wall_s += time.perf_counter() - t0
+        gpu_ms += e0.elapsed_time(e1)
         for j in range(seg):
             st = states[(done + j) % len(states)]
-            per_launch.append(ev[j].elapsed_time(ev[j + 1]))
             alg.append(algorithmic_bytes(w, st[3], st[4]))
             scan.append(scanned_bytes(w, st[3]))
         done += seg
-    return total_s, per_launch, alg, scan
+    return wall_s, gpu_ms, alg, scan
 
 
 # ---------------------------------------------------------------- oracle baseline
@@ -237,14 +240,13 @@ def main():
     t0 = time.perf_counter()
     states = prefill_states(w, min(pool, max(args.steps, 1)), dev)
     log(f"bench: states ready in {time.perf_counter() - t0:.1f} s; timing {args.steps} passes")
-    total_s, per_launch, alg, scan = time_pool(w, states, args.steps, args.warmup, dev)
-    ms_launch = float(np.mean(per_launch))
+    total_s, gpu_ms, alg, scan = time_pool(w, states, args.steps, args.warmup, dev)
+    ms_launch = gpu_ms / args.steps          # launch to launch, back to back
     passes_per_s = args.steps / total_s
-    kernel_s = sum(per_launch) / 1e3
+    kernel_s = gpu_ms / 1e3
     alg_gbps = sum(alg) / kernel_s / 1e9
     scan_gbps = sum(scan) / kernel_s / 1e9
-    log(f"bench: {passes_per_s:.1f} passes/s wall, mean launch {ms_launch * 1e3:.1f} us, "
-        f"min {min(per_launch) * 1e3:.1f} us, max {max(per_launch) * 1e3:.1f} us")
+    log(f"bench: {passes_per_s:.1f} passes/s wall, {ms_launch * 1e3:.2f} us per launch (HIP events)")
     traffic = load_traffic(w.name)
     out = {
         "metric": METRIC,

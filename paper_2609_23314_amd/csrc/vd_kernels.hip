@@ -33,6 +33,9 @@
 namespace vd {
 namespace {
 
+template <int V> struct IntC { static constexpr int value = V; };
+template <bool V> struct BoolC { static constexpr bool value = V; };
+
 constexpr int NT = kBlock;
 constexpr int NW = kWaves;
 constexpr int kUnroll = 4;  // 16-byte loads per lane per tile (two tiles in flight)
@@ -700,63 +703,94 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
         const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
         auto vfetch = [&](int r) -> uint4 {
-            return (stashed && r >= count)
-                       ? sfetch(r, cl)
-                       : *reinterpret_cast<const uint4 *>(vb + (int64_t)r * ss + cl * 16);
+            return (stashed && r >= count) ? sfetch(r, cl) : load_stream(vb + (int64_t)r * ss + cl * 16);
         };
         double acc[S::EPL];
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
         if (!st || steady) {
-            // Only the moved rows are touched.  All list reads come first, then
-            // every row load is issued unconditionally (indices clamped into the
-            // list), then the stores: no load waits behind another.
+            // Only the moved rows are touched.  A wave takes only the slots of a
+            // batch that hold a moved row for it, so no load is spent on padding;
+            // the list reads come first, then every row load of the batch, then
+            // the stores, with no load waiting behind another.
             const char *ksrc = kb ? kb : vb;  // without K a V row stands in, unused
-            for (int e0 = 0; e0 < n_moves; e0 += S::STEP) {
-                int dst[kUnroll], src[kUnroll];
+            const int wrow = wave_id() * S::RPW;
+            auto batch = [&](int e0, auto kvc, auto stashc) {
+                constexpr int KV = decltype(kvc)::value;
+                constexpr bool STASH = decltype(stashc)::value;
+                int dst[KV], src[KV];
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) {
+                for (int k = 0; k < KV; ++k) {
                     const int e = e0 + k * S::GROUPS + g;
                     const int ec = e < n_moves ? e : n_moves - 1;
                     dst[k] = (int)evl[ec];
                     src[k] = (int)mvl[ec];
                 }
-                uint4 vh[kUnroll], km[kUnroll], vm[kUnroll];
-                int32_t ps[kUnroll];
+                uint4 vh[KV], km[KV], vm[KV];
+                int32_t ps[KV];
+                // Row loads in the order their data is needed: the moved K and V
+                // rows feed the stores, the hole rows only the running sum.  They
+                // are non-temporal (scattered rows read once gain nothing from L2
+                // allocation and, measured, move markedly slower with it), and all
+                // are unconditional (without a state a hole row is read and
+                // ignored) so that no use can be hoisted next to its load.
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k)
-                    km[k] = *reinterpret_cast<const uint4 *>(ksrc + (int64_t)src[k] * ss + cl * 16);
-                if (st) {
+                for (int k = 0; k < KV; ++k)
+                    km[k] = load_stream(ksrc + (int64_t)src[k] * ss + cl * 16);
+                if constexpr (!STASH) {
 #pragma unroll
-                    for (int k = 0; k < kUnroll; ++k)
-                        vh[k] = *reinterpret_cast<const uint4 *>(vb + (int64_t)dst[k] * ss + cl * 16);
+                    for (int k = 0; k < KV; ++k) vm[k] = load_stream(vb + (int64_t)src[k] * ss + cl * 16);
                 }
                 if (pos) {
 #pragma unroll
-                    for (int k = 0; k < kUnroll; ++k) ps[k] = pos[src[k]];
-                }
-                if (stashed) {
-#pragma unroll
-                    for (int k = 0; k < kUnroll; ++k) vm[k] = sfetch(src[k], cl);
-                } else {
-#pragma unroll
-                    for (int k = 0; k < kUnroll; ++k)
-                        vm[k] = *reinterpret_cast<const uint4 *>(vb + (int64_t)src[k] * ss + cl * 16);
+                    for (int k = 0; k < KV; ++k) ps[k] = pos[src[k]];
                 }
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) {
+                for (int k = 0; k < KV; ++k) vh[k] = load_stream(vb + (int64_t)dst[k] * ss + cl * 16);
+                if constexpr (STASH) {
+#pragma unroll
+                    for (int k = 0; k < KV; ++k) vm[k] = sfetch(src[k], cl);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int k = 0; k < KV; ++k) {
                     const int e = e0 + k * S::GROUPS + g;
                     if (e >= n_moves) continue;
-                    if (st) {  // new sum = old - holes + movers
+                    if (kb) store_stream(kb + (int64_t)dst[k] * ss + cl * 16, km[k]);
+                    store_stream(vw + (int64_t)dst[k] * ss + cl * 16, vm[k]);
+                    if (pos && cl == 0) pos[dst[k]] = ps[k];
+                }
+                if (st) {  // new sum = old - holes + movers
+#pragma unroll
+                    for (int k = 0; k < KV; ++k) {
+                        const int e = e0 + k * S::GROUPS + g;
+                        if (e >= n_moves) continue;
                         float x[S::EPL], y[S::EPL];
                         E::unpack(vh[k], x);
                         E::unpack(vm[k], y);
 #pragma unroll
                         for (int i = 0; i < S::EPL; ++i) acc[i] += (double)y[i] - (double)x[i];
                     }
-                    if (kb) store_stream(kb + (int64_t)dst[k] * ss + cl * 16, km[k]);
-                    store_stream(vw + (int64_t)dst[k] * ss + cl * 16, vm[k]);
-                    if (pos && cl == 0) pos[dst[k]] = ps[k];
+                }
+            };
+            static_assert(kUnroll == 4, "the batch dispatch below covers 1..4 slots");
+            using I1 = IntC<1>;
+            using I2 = IntC<2>;
+            using I3 = IntC<3>;
+            using I4 = IntC<4>;
+            for (int e0 = 0; e0 < n_moves; e0 += S::STEP) {
+                const int left = n_moves - e0 - wrow;  // slot k holds a row for this wave iff k*GROUPS < left
+                const int kv = left <= 0 ? 0 : min(kUnroll, (left + S::GROUPS - 1) / S::GROUPS);
+                if (stashed) {
+                    if (kv == 4) batch(e0, I4{}, BoolC<true>{});
+                    else if (kv == 3) batch(e0, I3{}, BoolC<true>{});
+                    else if (kv == 2) batch(e0, I2{}, BoolC<true>{});
+                    else if (kv == 1) batch(e0, I1{}, BoolC<true>{});
+                } else {
+                    if (kv == 4) batch(e0, I4{}, BoolC<false>{});
+                    else if (kv == 3) batch(e0, I3{}, BoolC<false>{});
+                    else if (kv == 2) batch(e0, I2{}, BoolC<false>{});
+                    else if (kv == 1) batch(e0, I1{}, BoolC<false>{});
                 }
             }
         } else {
@@ -770,8 +804,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                     vh[k] = vfetch((int)evl[ec]);
                     if (ec < n_moves) {
                         const int src = (int)mvl[ec];
-                        km[k] = kb ? *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16)
-                                   : make_uint4(0u, 0u, 0u, 0u);
+                        km[k] = kb ? load_stream(kb + (int64_t)src * ss + cl * 16) : make_uint4(0u, 0u, 0u, 0u);
                         vm[k] = vfetch(src);
                     }
                 }
@@ -900,12 +933,10 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     for (int e = g; e < moves; e += S::GROUPS) {
         const int dst = (int)holes[e];
         const int src = (int)movers[e];
-        if (kb) {
-            const uint4 kv = *reinterpret_cast<const uint4 *>(kb + (int64_t)src * ss + cl * 16);
-            *reinterpret_cast<uint4 *>(kb + (int64_t)dst * ss + cl * 16) = kv;
-        }
-        const uint4 vv = *reinterpret_cast<const uint4 *>(vb + (int64_t)src * ss + cl * 16);
-        *reinterpret_cast<uint4 *>(vb + (int64_t)dst * ss + cl * 16) = vv;
+        const uint4 kv = kb ? load_stream(kb + (int64_t)src * ss + cl * 16) : make_uint4(0u, 0u, 0u, 0u);
+        const uint4 vv = load_stream(vb + (int64_t)src * ss + cl * 16);
+        if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, kv);
+        store_stream(vb + (int64_t)dst * ss + cl * 16, vv);
         if (pos && cl == 0) pos[dst] = pos[src];
     }
 }
