@@ -461,6 +461,149 @@ __device__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &
     return (int)mv_tot;
 }
 
+// Threshold and lists for the fused pass, with five block barriers on the
+// usual path.  Before the barrier that ends scoring, every wave has stored its
+// key minimum in bc[w] and maximum in bc[16 + w], and the histogram, the
+// candidate counter bc[100] and the keep mask bc[102..103] are zero.  Each
+// histogram pass is scanned by every wave on its own (the bin holding the N-th
+// largest key is found without a further barrier); once that bin holds at
+// most kCand keys, one sweep over the wave's slot segment counts the sure
+// decisions (below / above the bin) and collects the bin's keys, the waves
+// rank those candidates by (key desc, slot asc) between them, and each wave
+// writes its part of the lists.  Many equal keys at the
+// threshold (more than kCand) fall back to build_lists, which ranks them by
+// slot.  Lists and keep_out as in build_lists; returns the number of movers.
+__device__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
+                                uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H) {
+    const int w = wave_id(), lane = lane_id();
+    uint32_t lo = H.bc[0], hi = H.bc[16];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) {
+        lo = min(lo, H.bc[i]);
+        hi = max(hi, H.bc[16 + i]);
+    }
+    int need = N;
+    int in_range = n;
+    for (int pass = 0; in_range > kCand; ++pass) {
+        if (lo == hi) {  // more than kCand equal keys hold the threshold
+            __syncthreads();  // bc[0..31] has been read by every wave; build_lists reuses bc
+            return build_lists(keys, n, N, Threshold{lo, need, in_range}, evl, evict_cap, mvl,
+                               move_cap, keep_out, H);
+        }
+        if (pass > 0) {  // every wave has read the previous histogram
+            __syncthreads();
+            H.hist[threadIdx.x] = 0u;  // NT == kBins
+            __syncthreads();
+        }
+        const int bits = 32 - __clz(hi - lo);  // bits of the largest offset
+        const int shift = bits > 10 ? bits - 10 : 0;
+        for (int j = threadIdx.x; j < n; j += NT) {
+            const uint32_t k = keys[j];
+            if (k >= lo && k <= hi) atomicAdd(&H.hist[(k - lo) >> shift], 1u);
+        }
+        __syncthreads();
+        // wave w owns bins kBins-1-64w .. kBins-64-64w (descending keys)
+        const uint32_t total = wave_incl_scan(H.hist[kBins - 1 - threadIdx.x]);
+        if (lane == 63) H.bc[80 + w] = total;
+        __syncthreads();
+        const uint32_t un = (uint32_t)need;
+        const uint32_t wt = lane < NW ? H.bc[80 + lane] : 0u;
+        const uint32_t wincl = wave_incl_scan(wt);
+        // the wave holding it (the totals sum to in_range >= need, so one lane qualifies)
+        const int tw = max(__ffsll(__ballot(lane < NW && wincl >= un)) - 1, 0);
+        const uint32_t before = lane_u32(wincl - wt, tw);
+        const uint32_t hb = H.hist[kBins - 1 - (tw * 64 + lane)];
+        const uint32_t bincl = wave_incl_scan(hb) + before;
+        const int tl = max(__ffsll(__ballot(bincl >= un)) - 1, 0);
+        const uint32_t h = lane_u32(hb, tl);
+        const uint32_t above = lane_u32(bincl, tl) - h;
+        const uint64_t b = (uint64_t)(kBins - 1 - (tw * 64 + tl));
+        need -= (int)above;
+        in_range = (int)h;
+        const uint64_t top = (uint64_t)lo + ((b + 1) << shift) - 1u;
+        hi = top < (uint64_t)hi ? (uint32_t)top : hi;
+        lo = lo + (uint32_t)(b << shift);
+    }
+    // one sweep: sure evictions (below lo), sure movers (above hi, slot >= N),
+    // and the candidates in [lo, hi]
+    const int seg = (((n + NW - 1) / NW) + 63) & ~63;
+    const int j0 = w * seg;
+    const int j1 = min(n, j0 + seg);
+    uint32_t c_lo = 0, c_mv = 0;
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool valid = j < j1;
+        const uint32_t k = valid ? keys[j] : 0u;
+        const bool below = valid && k < lo;
+        const bool over = valid && k > hi;
+        c_lo += __popcll(__ballot(below));
+        c_mv += __popcll(__ballot(over && j >= N));
+        if (valid && !below && !over) {
+            const uint32_t slot = atomicAdd(&H.bc[100], 1u);
+            if (slot < (uint32_t)kCand) {  // the bin holds exactly in_range <= kCand keys
+                H.cand_key[slot] = k;
+                H.cand_idx[slot] = (uint32_t)j;
+            }
+        }
+    }
+    if (lane == 0) {
+        H.bc[32 + w] = c_lo;
+        H.bc[48 + w] = c_mv;
+    }
+    __syncthreads();
+    // lane t holds candidate t; wave w ranks candidates w, w+16, w+32, w+48 with
+    // one ballot each and records the kept ones in the mask bc[102..103]
+    const int c = in_range;
+    const bool live = lane < c;
+    const uint32_t ck = live ? H.cand_key[lane] : 0u;
+    const uint32_t ci = live ? H.cand_idx[lane] : 0u;
+    for (int i = w; i < c; i += NW) {
+        const uint32_t ki = lane_u32(ck, i), ji = lane_u32(ci, i);
+        const uint32_t rank = __popcll(__ballot(live && (ck > ki || (ck == ki && ci < ji))));
+        if (lane == 0 && rank < (uint32_t)need) atomicOr(&H.bc[102 + (i >> 5)], 1u << (i & 31));
+    }
+    __syncthreads();
+    const uint64_t keep_mask = ((uint64_t)H.bc[103] << 32) | H.bc[102];
+    const bool ckeep = (keep_mask >> lane) & 1ull;
+    const uint32_t mine_lo = (uint32_t)j0;  // candidates of earlier segments have smaller slots
+    uint32_t ev_off = __popcll(__ballot(live && !ckeep && ci < mine_lo));
+    uint32_t mv_off = __popcll(__ballot(live && ckeep && ci >= (uint32_t)N && ci < mine_lo));
+    uint32_t mv_tot = __popcll(__ballot(ckeep && ci >= (uint32_t)N));
+#pragma unroll
+    for (int i = 0; i < NW; ++i) {
+        const uint32_t e = H.bc[32 + i], m = H.bc[48 + i];
+        ev_off += i < w ? e : 0u;
+        mv_off += i < w ? m : 0u;
+        mv_tot += m;
+    }
+    for (int jb = j0; jb < j1; jb += 64) {
+        const int j = jb + lane;
+        const bool valid = j < j1;
+        const uint32_t k = valid ? keys[j] : 0u;
+        bool keep = valid && k > hi;
+        uint64_t mi = __ballot(valid && k >= lo && k <= hi);
+        while (mi) {  // slots in the bin take their candidate's decision
+            const int bl = __ffsll((unsigned long long)mi) - 1;
+            mi &= mi - 1;
+            const uint32_t jj = lane_u32((uint32_t)j, bl);
+            const int t = __ffsll(__ballot(live && ci == jj)) - 1;  // its candidate lane
+            if (lane == bl) keep = t >= 0 && ((keep_mask >> t) & 1ull);
+        }
+        const bool ev = valid && !keep;
+        const bool mv = valid && keep && j >= N;
+        const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
+        const uint32_t rev = ev_off + __popcll(mev & lanes_below());
+        const uint32_t rmv = mv_off + __popcll(mmv & lanes_below());
+        if (ev && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
+        if (mv && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
+        if (keep_out && valid) keep_out[j] = keep ? 1 : 0;
+        ev_off += __popcll(mev);
+        mv_off += __popcll(mmv);
+    }
+    __syncthreads();
+    return (int)mv_tot;
+}
+
 // ---------------------------------------------------------------- the pass
 
 template <int DT, int D, int VAR>
@@ -655,6 +798,16 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
         }
     }
+    if (to_lds) {  // what the selection reads after the barrier below
+        kmin = wave_min_u32(kmin);
+        kmax = wave_max_u32(kmax);
+        if (lane == 0) {
+            H.bc[wave_id()] = kmin;
+            H.bc[16 + wave_id()] = kmax;
+        }
+        H.hist[threadIdx.x] = 0u;  // NT == kBins
+        if (threadIdx.x < 4) H.bc[100 + threadIdx.x] = 0u;  // candidate count, keep mask
+    }
     __syncthreads();
     if (score_mode) return;
 
@@ -684,8 +837,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = j == victim ? 0 : 1;
             __syncthreads();
         } else {
-            const Threshold th = select_threshold(keys, n, N, kmin, kmax, H);
-            n_moves = build_lists(keys, n, N, th, evl, p.evict_cap, mvl, p.move_cap, keep_out, H);
+            n_moves = select_and_build(keys, n, N, evl, p.evict_cap, mvl, p.move_cap, keep_out, H);
         }
     } else {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;

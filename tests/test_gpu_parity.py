@@ -216,6 +216,32 @@ def test_step_ties_zero_and_duplicate_rows(orc, variant):
                  per_unit(N, L, H), variant, torch.bfloat16, scores_gpu=sg, keep_gpu=kg)
 
 
+@pytest.mark.parametrize("variant", ["l2", "norm"])
+def test_step_clustered_scores_with_outliers(orc, variant):
+    """A few huge and tiny rows stretch the key range, so the bin holding the
+    threshold after the first histogram pass still holds hundreds of keys and
+    the selection narrows it again."""
+    S, L, H, C, D = 1, 1, 2, 2000, 128
+    n, N = [2000], [1000]
+    k, v = make_cache(S, L, H, C, D, torch.float32, n, seed=97, nan_tail=False)
+    g = torch.Generator(device="cpu").manual_seed(98)
+    big = (torch.randn(5, D, generator=g) * 1e3).to(DEV)
+    v[0, 0, 0, 0:10:2] = big                 # +x and -x pairs keep the mean small
+    v[0, 0, 0, 1:10:2] = -big
+    v[0, 0, 0, 10:15] = (torch.randn(5, D, generator=g) * 1e-4).to(DEV)
+    U = S * L * H
+    pre_k, pre_v = units(to_np(k)), units(to_np(v))
+    scores = torch.zeros((U, C), device=DEV)
+    keep = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
+    vd.vd_evict_step(k, v, n, N, variant, scores_out=scores, keep_out=keep)
+    torch.cuda.synchronize()
+    kg = to_np(keep)
+    assert kg[0, :10].all(), "the outlier rows score highest"
+    compare_pass(orc, pre_k, pre_v, units(to_np(k)), units(to_np(v)), per_unit(n, L, H),
+                 per_unit(N, L, H), variant, torch.float32, scores_gpu=to_np(scores),
+                 keep_gpu=kg)
+
+
 def test_step_tiny_units(orc):
     """n = 0, n = 1, N = 1 and n == N in one launch."""
     run_step_case(orc, 5, 1, 1, 8, 64, torch.float32, n=[0, 1, 2, 8, 5], N=[1, 1, 1, 8, 2],
