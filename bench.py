@@ -154,17 +154,69 @@ def time_pool(w, states, steps, warmup, dev):
     return wall_s, gpu_ms, alg, scan
 
 
+def decode_state(w: synth.Workload, dev):
+    """A decode step of every sequence: N old tokens and one new token in the
+    cache (n = N + 1), and the running sum of the N old rows."""
+    S, L, H, D = w.num_seqs, w.num_layers, w.num_kv_heads, w.head_dim
+    k, v = synth.empty_cache(w, dev)
+    rs = torch.zeros((w.units, D + 1), dtype=torch.float64, device=dev)
+    for s in range(S):
+        N = w.budget[s]
+        k[s, :, :, :N + 1] = synth.block_rows(w, "k", s, 0, 0, N + 1, dev, seq_seed=s)
+        v[s, :, :, :N + 1] = synth.block_rows(w, "v", s, 0, 0, N + 1, dev, seq_seed=s)
+        us = slice(s * L * H, (s + 1) * L * H)
+        rs[us, :D] = v[s, :, :, :N].double().sum(dim=2).reshape(L * H, D)
+        rs[us, D] = N
+    return k, v, rs, [N + 1 for N in w.budget]
+
+
+def time_in_place(w, k, v, rs, n, steps, warmup, dev):
+    """Decode passes replayed on one cache: after a pass the valid slots are
+    [0, N) and slot N still holds a row, so the next call with n = N + 1 is
+    again a well-formed decode step (its new token is that row).  Returns
+    (wall seconds, GPU milliseconds) of `steps` back-to-back passes."""
+    for _ in range(warmup):
+        vd.vd_evict_step(k, v, n, w.budget, "l2", running_sum=rs)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(steps):
+        vd.vd_evict_step(k, v, n, w.budget, "l2", running_sum=rs)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0, e0.elapsed_time(e1)
+
+
+def decode_movers(w, k, v, rs, n, dev):
+    """Moved rows per unit of one decode pass (run on copies, untimed)."""
+    keep = torch.zeros((w.units, w.capacity), dtype=torch.uint8, device=dev)
+    vd.vd_evict_step(k.clone(), v.clone(), n, w.budget, "l2", running_sum=rs.clone(),
+                     keep_out=keep)
+    L, H = w.num_layers, w.num_kv_heads
+    out = []
+    for s in range(w.num_seqs):
+        N = w.budget[s]
+        out.append(int(keep[s * L * H:(s + 1) * L * H, N].sum().item()))
+    return out
+
+
 # ---------------------------------------------------------------- oracle baseline
 
-def cpu_baseline(w, state, budget_s=10.0):
-    """The oracle on the host cores: whole passes over one pre-pass state."""
+def cpu_baseline(w, state, budget_s=10.0, max_units=None):
+    """The oracle on the host cores: whole passes over one pre-pass state, or
+    over its first `max_units` units (then scaled to whole passes)."""
     import oracle
     k, v, _, n, _ = state
     S, L, H, C, D = k.shape
-    kn = to_np(k).reshape(S * L * H, C, D)
-    vn = to_np(v).reshape(S * L * H, C, D)
-    nu = np.repeat(np.asarray(n, np.int32), L * H)
-    Nu = np.repeat(np.asarray(w.budget, np.int32), L * H)
+    U = S * L * H
+    take = U if max_units is None else min(U, max_units)
+    kn = to_np(k.reshape(U, C, D)[:take])
+    vn = to_np(v.reshape(U, C, D)[:take])
+    nu = np.repeat(np.asarray(n, np.int32), L * H)[:take]
+    Nu = np.repeat(np.asarray(w.budget, np.int32), L * H)[:take]
     threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
     orc = oracle.load()
     elapsed, reps = 0.0, 0
@@ -174,10 +226,13 @@ def cpu_baseline(w, state, budget_s=10.0):
         orc.evict_step(kc, vc, nu, Nu, "l2", nthreads=threads)
         elapsed += time.perf_counter() - t0
         reps += 1
-    return {"value": reps / elapsed, "unit": "passes/s", "cores": threads, "kind": "oracle",
-            "sample": f"{reps} whole passes of one {w.name} boundary ({w.units} units, "
-                      f"n={max(n)}) in {elapsed:.1f} s",
-            "gbps_scanned": reps * scanned_bytes(w, n) / elapsed / 1e9}
+    frac = take / U
+    what = (f"{reps} whole passes of one {w.name} boundary ({U} units, n={max(n)})" if take == U
+            else f"{reps} passes over {take} of the {U} units of one {w.name} step "
+                 f"(n={max(n)}), scaled to whole passes")
+    return {"value": reps * frac / elapsed, "unit": "passes/s", "cores": threads,
+            "kind": "oracle", "sample": f"{what} in {elapsed:.1f} s",
+            "gbps_scanned": reps * frac * scanned_bytes(w, n) / elapsed / 1e9}
 
 
 def to_np(t):
@@ -208,7 +263,9 @@ def main():
     ap.add_argument("--steps", type=int, default=60)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llama3_8b_prefill",
-                    choices=["llama3_8b_prefill", "wide_head_d256"])
+                    choices=["llama3_8b_prefill", "wide_head_d256", "decode_b16",
+                             "ragged_serving"],
+                    help="the last two time decode steps (n = N + 1 in every sequence)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -235,12 +292,24 @@ def main():
         return
     vd.load()
     w = synth.WORKLOADS[args.workload]()
-    pool = 60 if w.name == "llama3_8b_prefill" else 8
-    log(f"bench: building {pool} pre-pass states of {w.name} ...")
-    t0 = time.perf_counter()
-    states = prefill_states(w, min(pool, max(args.steps, 1)), dev)
-    log(f"bench: states ready in {time.perf_counter() - t0:.1f} s; timing {args.steps} passes")
-    total_s, gpu_ms, alg, scan = time_pool(w, states, args.steps, args.warmup, dev)
+    decode = args.workload in ("decode_b16", "ragged_serving")
+    if decode:
+        log(f"bench: building the {w.name} decode cache ({w.units} units) ...")
+        k, v, rs, n = decode_state(w, dev)
+        movers = decode_movers(w, k, v, rs, n, dev)
+        log(f"bench: timing {args.steps} decode passes in place")
+        total_s, gpu_ms = time_in_place(w, k, v, rs, n, args.steps, args.warmup, dev)
+        alg = [algorithmic_bytes(w, n, movers)] * args.steps
+        scan = [scanned_bytes(w, n)] * args.steps
+        base_state = (k, v, rs, n, movers)
+    else:
+        pool = 60 if w.name == "llama3_8b_prefill" else 8
+        log(f"bench: building {pool} pre-pass states of {w.name} ...")
+        t0 = time.perf_counter()
+        states = prefill_states(w, min(pool, max(args.steps, 1)), dev)
+        log(f"bench: states ready in {time.perf_counter() - t0:.1f} s; timing {args.steps} passes")
+        total_s, gpu_ms, alg, scan = time_pool(w, states, args.steps, args.warmup, dev)
+        base_state = states[0]
     ms_launch = gpu_ms / args.steps          # launch to launch, back to back
     passes_per_s = args.steps / total_s
     kernel_s = gpu_ms / 1e3
@@ -263,8 +332,11 @@ def main():
         "data": "synthetic (seeded generator; no model weights or datasets)",
         "config": {"workload": w.name, "seqs": w.num_seqs, "layers": w.num_layers,
                    "kv_heads": w.num_kv_heads, "q_heads": w.num_q_heads,
-                   "head_dim": w.head_dim, "budget": w.budget[0], "block": w.block,
-                   "prompt": w.prompt[0], "n": max(states[0][3]), "variant": "l2",
+                   "head_dim": w.head_dim,
+                   "budget": (w.budget[0] if len(set(w.budget)) == 1
+                              else [min(w.budget), max(w.budget)]),
+                   "block": w.block,
+                   "prompt": max(w.prompt), "n": max(base_state[3]), "variant": "l2",
                    "running_sum": True, "parallelism": "single GPU"},
         "kv_gbps_scanned": round(scan_gbps, 1),
         "kv_scan_frac_of_hbm_peak": round(scan_gbps / HBM_PEAK_GBPS, 4),
@@ -273,13 +345,14 @@ def main():
                      "traffic": None if traffic is None else int(traffic),
                      "traffic_over_alg": (None if traffic is None else
                                           round(traffic / (sum(alg) / len(alg)), 3)),
-                     "kernel": "step_kernel<bf16,128,L2>",
+                     "kernel": f"step_kernel<bf16,{w.head_dim},L2>",
                      "launch_us": round(ms_launch * 1e3, 2),
                      "alg_bytes_per_launch": int(np.mean(alg))},
     }
     if not args.no_cpu_baseline:
         log("bench: timing the oracle on the host ...")
-        out["cpu_baseline"] = cpu_baseline(w, states[0], args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, base_state, args.cpu_seconds,
+                                           max_units=64 if decode else None)
     print(json.dumps(out), flush=True)
 
 
