@@ -83,7 +83,7 @@ vd_status plan_step_lds(const vd_cache_desc *d, UnitParams &p, int ns, bool scor
         const int n = p.n[i], N = p.N[i];
         nmax = std::max(nmax, n);
         if (!score_mode && n > N) {
-            if (n > N + 1) keys_cap = std::max(keys_cap, n);
+            keys_cap = std::max(keys_cap, n);
             evict_cap = std::max(evict_cap, n - N);
             move_cap = std::max(move_cap, std::min(N, n - N));
             want_rows = std::max(want_rows, have_state ? n - N : n);

@@ -153,6 +153,27 @@ __device__ __forceinline__ void store_stream(char *p, uint4 v) {
     __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
 }
 
+// Square root and reciprocal square root of the scores: the hardware
+// instructions (within one unit in the last place) without the exact-rounding
+// fix-up sequence.  Subnormal inputs are scaled by 2^64 first, since the
+// hardware units do not take them.  Every score of the library goes through
+// these two, so the standalone and the fused paths agree bit for bit.
+__device__ __forceinline__ float score_sqrt(float x) {
+    const bool tiny = x < 1.17549435e-38f;  // below the smallest normal
+    const float r = __builtin_amdgcn_sqrtf(tiny ? x * 18446744073709551616.0f : x);
+    return tiny ? r * 2.3283064365386963e-10f : r;  // 2^-32
+}
+__device__ __forceinline__ float score_rsqrt(float x) {
+    const bool tiny = x < 1.17549435e-38f;
+    const float r = __builtin_amdgcn_rsqf(tiny ? x * 18446744073709551616.0f : x);
+    return tiny ? r * 4294967296.0f : r;  // 2^32
+}
+
+// Order-preserving key of a score: scores are never negative (sums of squares
+// and their roots, or half a squared distance), and for non-negative floats
+// (+0 and -0 alike) setting the sign bit preserves the order.
+__device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s) | 0x80000000u; }
+
 // Order-preserving map of an fp32 value onto uint32 (-0 taken as +0).
 __device__ __forceinline__ uint32_t orderable(float f) {
     uint32_t b = __float_as_uint(f);
@@ -208,6 +229,30 @@ __device__ __forceinline__ void for_rows_pre2(int count, RowOf row_of, Fetch fet
         load_tile<DT, D>(t + 3, count, row_of, fetch, b);
     }
     if (t < ntiles) use_tile<DT, D>(t, count, a, body);
+}
+
+// As for_rows_pre2 with four tiles in flight: tiles 0..3 are already loaded
+// in a, b, c and d.
+template <int DT, int D, typename RowOf, typename Fetch, typename Body>
+__device__ __forceinline__ void for_rows_pre4(int count, RowOf row_of, Fetch fetch, Body body,
+                                              uint4 (&a)[kUnroll], uint4 (&b)[kUnroll],
+                                              uint4 (&c)[kUnroll], uint4 (&d)[kUnroll]) {
+    using S = Shape<DT, D>;
+    const int ntiles = (count + S::STEP - 1) / S::STEP;
+    int t = 0;
+    for (; t + 3 < ntiles; t += 4) {
+        use_tile<DT, D>(t, count, a, body);
+        load_tile<DT, D>(t + 4, count, row_of, fetch, a);
+        use_tile<DT, D>(t + 1, count, b, body);
+        load_tile<DT, D>(t + 5, count, row_of, fetch, b);
+        use_tile<DT, D>(t + 2, count, c, body);
+        load_tile<DT, D>(t + 6, count, row_of, fetch, c);
+        use_tile<DT, D>(t + 3, count, d, body);
+        load_tile<DT, D>(t + 7, count, row_of, fetch, d);
+    }
+    if (t < ntiles) use_tile<DT, D>(t, count, a, body);
+    if (t + 1 < ntiles) use_tile<DT, D>(t + 1, count, b, body);
+    if (t + 2 < ntiles) use_tile<DT, D>(t + 2, count, c, body);
 }
 
 // Loads the first two tiles of a stream (clamped like every other tile).
@@ -672,8 +717,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss));
         if (probe == 0x7FC00001u) H.bc[127] = probe;  // keeps the load; nothing reads bc[127]
     }
-    const bool to_lds = evict && !amode;
-    uint64_t best = ~0ull;                    // (key << 32) | ~slot: min = lowest score, highest slot
+    const bool to_lds = evict;  // keys of every evicting unit go to LDS
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
     float m[S::EPL];                          // this lane's columns of v_bar (Dir: v_bar / |v_bar|)
     bool mean_zero = false;
@@ -733,19 +777,19 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 const float t = x[i] - m[i];
                 a = fmaf(t, t, a);
             }
-            s = sqrtf(row_sum<S::LPR>(a));
+            s = score_sqrt(row_sum<S::LPR>(a));
         } else if constexpr (VAR == 2) {  // Norm: ||v||
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
-            s = sqrtf(row_sum<S::LPR>(a));
+            s = score_sqrt(row_sum<S::LPR>(a));
         } else {  // Dir: 1 - cos = ||v/|v| - v_bar/|v_bar| ||^2 / 2
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
             const float nv2 = row_sum<S::LPR>(a);
             const bool ok = nv2 > 0.f && !mean_zero;
-            const float inv = ok ? 1.0f / sqrtf(nv2) : 0.f;
+            const float inv = ok ? score_rsqrt(nv2) : 0.f;
             float b = 0.f;
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) {
@@ -756,15 +800,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             s = ok ? half : 1.0f;
         }
         if (cl == 0 && valid) {
-            const uint32_t key = orderable(s);
+            const uint32_t key = score_key(s);
             if (to_lds) {
                 keys[r] = key;
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
-            }
-            if (amode) {
-                const uint64_t c = ((uint64_t)key << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)r);
-                best = c < best ? c : best;
             }
             if (scores_out) scores_out[r] = s;
         }
@@ -815,6 +855,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     int n_moves = 0;
     if (evict) {
         if (amode) {
+            // (key << 32) | ~slot: the minimum is the lowest score, highest slot
+            uint64_t best = ~0ull;
+            for (int j = threadIdx.x; j < n; j += NT) {
+                const uint64_t c = ((uint64_t)keys[j] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
+                best = c < best ? c : best;
+            }
             best = wave_min_u64(best);
             if (lane == 0) {
                 H.bc[2 * wave_id()] = (uint32_t)(best >> 32);
