@@ -694,11 +694,29 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         return;
     }
 
-    int count = 0;
-    if (st) {
-        const double c = st[D];
-        count = (c >= 0.0 && c <= (double)n && c == (double)(int)c) ? (int)c : 0;
+    // The state's token count says which rows are new: [count, n).  It is read
+    // first; in steady state it equals N, so the loads of rows [min(N, n), n)
+    // go out right behind it instead of waiting for it (path A below uses them
+    // only if the guess holds).  Every load here is unconditional, so each later
+    // wait counts exactly.
+    const double craw = *(st ? st + D : reinterpret_cast<const double *>(vb));
+    const int guess = min(N, n);
+    const bool spec = st && guess > 0 && n - guess > 0 && n - guess <= 2 * S::STEP;
+    uint4 new_a[kUnroll], new_b[kUnroll];
+    {
+        const int gb = spec ? guess : n - 1;   // otherwise one row, read and not used
+        auto guess_row = [&](int e) { return min(gb + e, n - 1); };
+        load_first2<DT, D>(spec ? n - guess : 1, guess_row,
+                           [&](int r, int c) { return load_stream(vb + (int64_t)r * ss + c * 16); },
+                           new_a, new_b);
     }
+    // one early read of the unit's K slab warms its address translation before
+    // the gather moves K rows; the value is only looked at after scoring
+    uint32_t kprobe = 0u;
+    if (evict && p.k && threadIdx.x == 0)
+        kprobe = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss));
+    int count = 0;
+    if (st) count = (craw >= 0.0 && craw <= (double)n && craw == (double)(int)craw) ? (int)craw : 0;
     const int fresh = n - count;
     const bool stashed = fresh <= p.stash_rows;
     auto gfetch = [&](int r, int c) -> uint4 { return load_stream(vb + (int64_t)r * ss + c * 16); };
@@ -710,13 +728,6 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     auto old_row = [&](int e) { return min(e, lastrow); };
     const bool score_old = need_scores && count > 0;
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
-    if (evict && p.k && threadIdx.x == 0) {
-        // one early read of the unit's K slab warms its address translation
-        // before the gather moves K rows; the value itself is not needed
-        const uint32_t probe = __builtin_nontemporal_load(
-            reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss));
-        if (probe == 0x7FC00001u) H.bc[127] = probe;  // keeps the load; nothing reads bc[127]
-    }
     const bool to_lds = evict;  // keys of every evicting unit go to LDS
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
     float m[S::EPL];                          // this lane's columns of v_bar (Dir: v_bar / |v_bar|)
@@ -811,14 +822,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     };
 
     auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
-    if (score_old && fresh <= 2 * S::STEP) {
-        // the new block fits two tiles: it is read alone (every CU's new rows
-        // then reach the memory controllers ahead of any old-row traffic), and
+    if (score_old && spec && count == guess) {
+        // path A: the new block fits two tiles and was loaded above (every CU's
+        // new rows reach the memory controllers ahead of any old-row traffic);
         // the first two tiles of the old rows go out as soon as it has landed,
         // to arrive while the mean is reduced
-        uint4 new_a[kUnroll], new_b[kUnroll], pre_a[kUnroll], pre_b[kUnroll];
-        const int fl = fresh > 0 ? fresh : 1;
-        load_first2<DT, D>(fl, fresh_row, gfetch, new_a, new_b);
+        uint4 pre_a[kUnroll], pre_b[kUnroll];
         use_tile<DT, D>(0, fresh, new_a, mean_body);
         use_tile<DT, D>(1, fresh, new_b, mean_body);
         __builtin_amdgcn_sched_barrier(0);
@@ -838,6 +847,10 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
         }
     }
+    // the probe value is consumed only here (the empty asm keeps the compiler
+    // from testing it, and so waiting for it, next to the load)
+    asm volatile("" : "+v"(kprobe));
+    if (kprobe == 0x7FC00001u) H.bc[127] = kprobe;  // keeps the probe load; nothing reads bc[127]
     if (to_lds) {  // what the selection reads after the barrier below
         kmin = wave_min_u32(kmin);
         kmax = wave_max_u32(kmax);
