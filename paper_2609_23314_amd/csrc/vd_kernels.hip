@@ -334,7 +334,7 @@ struct Threshold {
 // (key desc, slot asc).  A pass narrows the range 512-fold or more, so at most
 // four passes run.
 // kmin / kmax are this thread's partial minimum and maximum of the keys.
-__device__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32_t kmin,
+__device__ __forceinline__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32_t kmin,
                                       uint32_t kmax, LdsHead &H) {
     kmin = wave_min_u32(kmin);
     kmax = wave_max_u32(kmax);
@@ -434,7 +434,7 @@ __device__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32
 // (ascending) to evl and the kept slots >= N (ascending) to mvl; writes
 // keep_out if given.  Wave w owns a contiguous segment of slots, so only the
 // per-wave counts cross waves.  Returns the number of movers.
-__device__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &th,
+__device__ __forceinline__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &th,
                            uint32_t *evl, int evict_cap, uint32_t *mvl, int move_cap,
                            uint8_t *keep_out, LdsHead &H) {
     const int w = wave_id(), lane = lane_id();
@@ -518,7 +518,7 @@ __device__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &
 // writes its part of the lists.  Many equal keys at the
 // threshold (more than kCand) fall back to build_lists, which ranks them by
 // slot.  Lists and keep_out as in build_lists; returns the number of movers.
-__device__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
+__device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
                                 uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H) {
     const int w = wave_id(), lane = lane_id();
     uint32_t lo = H.bc[0], hi = H.bc[16];
