@@ -31,10 +31,13 @@ vd_status check_desc(const vd_cache_desc *d) {
     if (d->stride_seq < 0 || d->stride_layer < 0 || d->stride_head < 0 || d->stride_slot < 0)
         return VD_ERR_INVALID_ARG;
     if (d->stride_slot < d->head_dim) return VD_ERR_INVALID_ARG;  // rows would overlap
+    if (d->num_layers > 65535) return VD_ERR_UNSUPPORTED;  // one grid row per layer
     const int64_t units = int64_t(d->num_seqs) * d->num_layers * d->num_kv_heads;
     if (units > INT32_MAX || units * int64_t(d->capacity) > (int64_t(1) << 47))
         return VD_ERR_UNSUPPORTED;
     const int64_t es = elem_bytes(d->dtype);
+    // a unit's slab is addressed with 32-bit byte offsets
+    if (int64_t(d->capacity) * d->stride_slot * es > int64_t(UINT32_MAX)) return VD_ERR_UNSUPPORTED;
     const int64_t strides[4] = {d->stride_seq, d->stride_layer, d->stride_head, d->stride_slot};
     for (int64_t s : strides)
         if ((s * es) % 16 != 0) return VD_ERR_INVALID_ARG;  // every row 16-byte aligned
@@ -62,26 +65,27 @@ UnitParams base_params(const vd_cache_desc *d, int s0, int ns, const int32_t *n_
     p.s_seq = d->stride_seq * es;
     p.s_layer = d->stride_layer * es;
     p.s_head = d->stride_head * es;
-    p.s_slot = d->stride_slot * es;
+    p.s_slot = uint32_t(d->stride_slot * es);
     p.num_layers = d->num_layers;
     p.num_kv_heads = d->num_kv_heads;
     p.unit0 = s0 * d->num_layers * d->num_kv_heads;
     p.capacity = d->capacity;
     for (int i = 0; i < ns; ++i) {
-        p.n[i] = n_valid[s0 + i];
-        p.N[i] = budget ? budget[s0 + i] : INT32_MAX;
+        p.nN[2 * i] = n_valid[s0 + i];
+        p.nN[2 * i + 1] = budget ? budget[s0 + i] : INT32_MAX;
     }
     return p;
 }
 
 // Plans the dynamic LDS of the pass kernel for one launch.
 vd_status plan_step_lds(const vd_cache_desc *d, UnitParams &p, int ns, bool score_mode,
-                        bool have_state, size_t &lds_bytes) {
+                        bool have_state, bool want_scores, size_t &lds_bytes) {
     const int64_t row_bytes = int64_t(d->head_dim) * elem_bytes(d->dtype);
     int nmax = 0, keys_cap = 0, evict_cap = 0, move_cap = 0, want_rows = 0;
     for (int i = 0; i < ns; ++i) {
-        const int n = p.n[i], N = p.N[i];
+        const int n = p.nN[2 * i], N = p.nN[2 * i + 1];
         nmax = std::max(nmax, n);
+        if (want_scores) keys_cap = std::max(keys_cap, n);  // scores leave through LDS
         if (!score_mode && n > N) {
             keys_cap = std::max(keys_cap, n);
             evict_cap = std::max(evict_cap, n - N);
@@ -122,7 +126,6 @@ vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant
     if (variant < VD_SCORE_L2 || variant > VD_SCORE_NORM) return VD_ERR_INVALID_ARG;
     if (!scores || !aligned(scores, 4) || (mean_out && !aligned(mean_out, 4)))
         return VD_ERR_INVALID_ARG;
-    const int per_seq = desc->num_layers * desc->num_kv_heads;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, nullptr);
@@ -130,8 +133,8 @@ vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant
         p.scores = scores;
         p.mean_out = mean_out;
         size_t lds = 0;
-        if ((st = plan_step_lds(desc, p, ns, true, false, lds)) != VD_OK) return st;
-        st = launched(vd::launch_step(p, ns * per_seq, desc->dtype, desc->head_dim, variant, lds,
+        if ((st = plan_step_lds(desc, p, ns, true, false, true, lds)) != VD_OK) return st;
+        st = launched(vd::launch_step(p, ns, desc->dtype, desc->head_dim, variant, lds,
                                       reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;
     }
@@ -145,19 +148,18 @@ vd_status vd_select_topn(const vd_cache_desc *desc, const float *scores, const i
     if (!budget) return VD_ERR_INVALID_ARG;
     if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
     if (!scores || !keep_mask || !aligned(scores, 4)) return VD_ERR_INVALID_ARG;
-    const int per_seq = desc->num_layers * desc->num_kv_heads;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, budget);
         p.scores_in = scores;
         p.keep = keep_mask;
         int nmax = 0;
-        for (int i = 0; i < ns; ++i) nmax = std::max(nmax, p.n[i]);
+        for (int i = 0; i < ns; ++i) nmax = std::max(nmax, p.nN[2 * i]);
         p.off_keys = int32_t(sizeof(vd::LdsHead));
         p.keys_cap = nmax;
         const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(nmax) * 4));
         if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
-        st = launched(vd::launch_select(p, ns * per_seq, lds, reinterpret_cast<hipStream_t>(stream)));
+        st = launched(vd::launch_select(p, ns, lds, reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;
     }
     return VD_OK;
@@ -170,7 +172,6 @@ vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask, const 
     if (!budget) return VD_ERR_INVALID_ARG;
     if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
     if (!keep_mask || (pos && !aligned(pos, 4))) return VD_ERR_INVALID_ARG;
-    const int per_seq = desc->num_layers * desc->num_kv_heads;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, budget);
@@ -178,9 +179,10 @@ vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask, const 
         p.pos = pos;
         int holes = 0, movers = 0;
         for (int i = 0; i < ns; ++i) {
-            if (p.n[i] > p.N[i]) {
-                holes = std::max(holes, std::min(p.N[i], p.n[i]));
-                movers = std::max(movers, p.n[i] - p.N[i]);
+            const int n = p.nN[2 * i], N = p.nN[2 * i + 1];
+            if (n > N) {
+                holes = std::max(holes, std::min(N, n));
+                movers = std::max(movers, n - N);
             }
         }
         if (holes == 0) continue;  // nothing exceeds its budget in this launch
@@ -189,7 +191,7 @@ vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask, const 
         p.move_cap = movers;
         const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(holes + movers) * 4));
         if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
-        st = launched(vd::launch_compact(p, ns * per_seq, desc->dtype, desc->head_dim, lds,
+        st = launched(vd::launch_compact(p, ns, desc->dtype, desc->head_dim, lds,
                                          reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;
     }
@@ -210,7 +212,6 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const
     if ((running_sum && !aligned(running_sum, 8)) || (pos && !aligned(pos, 4)) ||
         (scores_out && !aligned(scores_out, 4)))
         return VD_ERR_INVALID_ARG;
-    const int per_seq = desc->num_layers * desc->num_kv_heads;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, budget);
@@ -220,9 +221,10 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const
         p.scores = scores_out;
         p.keep = keep_out;
         size_t lds = 0;
-        if ((st = plan_step_lds(desc, p, ns, false, running_sum != nullptr, lds)) != VD_OK)
+        if ((st = plan_step_lds(desc, p, ns, false, running_sum != nullptr, scores_out != nullptr,
+                                lds)) != VD_OK)
             return st;
-        st = launched(vd::launch_step(p, ns * per_seq, desc->dtype, desc->head_dim, variant, lds,
+        st = launched(vd::launch_step(p, ns, desc->dtype, desc->head_dim, variant, lds,
                                       reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;
     }

@@ -140,17 +140,24 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// Row addresses are a workgroup-uniform base plus a 32-bit byte offset (the
+// host checks that a unit's slab spans less than 4 GiB), so every access is a
+// scalar-base load or store with one offset register per lane.
+__device__ __forceinline__ uint32_t row_off(int r, uint32_t ss, int chunk) {
+    return (uint32_t)r * ss + (uint32_t)chunk * 16u;
+}
+
 // 16-byte load that bypasses cache retention: the value rows stream through once.
-__device__ __forceinline__ uint4 load_stream(const char *p) {
-    const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+__device__ __forceinline__ uint4 load_stream(const char *base, uint32_t off) {
+    const u32x4 t = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(base + off));
     return make_uint4(t.x, t.y, t.z, t.w);
 }
 
 // 16-byte store that is not kept in the cache: moved rows are not read again here.
-__device__ __forceinline__ void store_stream(char *p, uint4 v) {
+__device__ __forceinline__ void store_stream(char *base, uint32_t off, uint4 v) {
     u32x4 t;
     t.x = v.x; t.y = v.y; t.z = v.z; t.w = v.w;
-    __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
+    __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(base + off));
 }
 
 // Square root and reciprocal square root of the scores: the hardware
@@ -217,42 +224,30 @@ template <int DT, int D, typename RowOf, typename Fetch, typename Body>
 __device__ __forceinline__ void for_rows_pre2(int count, RowOf row_of, Fetch fetch, Body body,
                                               uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
     using S = Shape<DT, D>;
-    // Loads are issued unconditionally (past the end they re-read the last row),
-    // so every iteration leaves the same two tiles in flight and the in-order
-    // load counter lets each use wait for exactly its own tile.
+    // Two tiles stay in flight.  The loop only runs while both tiles it loads
+    // exist, and the last one to three tiles are taken in straight-line code:
+    // no load is issued past the end, and every use waits for exactly its own
+    // tile (the load counter retires in order).
     const int ntiles = (count + S::STEP - 1) / S::STEP;
     int t = 0;
-    for (; t + 1 < ntiles; t += 2) {
+    for (; t + 3 < ntiles; t += 2) {
         use_tile<DT, D>(t, count, a, body);
         load_tile<DT, D>(t + 2, count, row_of, fetch, a);
         use_tile<DT, D>(t + 1, count, b, body);
         load_tile<DT, D>(t + 3, count, row_of, fetch, b);
     }
-    if (t < ntiles) use_tile<DT, D>(t, count, a, body);
-}
-
-// As for_rows_pre2 with four tiles in flight: tiles 0..3 are already loaded
-// in a, b, c and d.
-template <int DT, int D, typename RowOf, typename Fetch, typename Body>
-__device__ __forceinline__ void for_rows_pre4(int count, RowOf row_of, Fetch fetch, Body body,
-                                              uint4 (&a)[kUnroll], uint4 (&b)[kUnroll],
-                                              uint4 (&c)[kUnroll], uint4 (&d)[kUnroll]) {
-    using S = Shape<DT, D>;
-    const int ntiles = (count + S::STEP - 1) / S::STEP;
-    int t = 0;
-    for (; t + 3 < ntiles; t += 4) {
+    const int left = ntiles - t;
+    if (left == 3) {
         use_tile<DT, D>(t, count, a, body);
-        load_tile<DT, D>(t + 4, count, row_of, fetch, a);
+        load_tile<DT, D>(t + 2, count, row_of, fetch, a);
         use_tile<DT, D>(t + 1, count, b, body);
-        load_tile<DT, D>(t + 5, count, row_of, fetch, b);
-        use_tile<DT, D>(t + 2, count, c, body);
-        load_tile<DT, D>(t + 6, count, row_of, fetch, c);
-        use_tile<DT, D>(t + 3, count, d, body);
-        load_tile<DT, D>(t + 7, count, row_of, fetch, d);
+        use_tile<DT, D>(t + 2, count, a, body);
+    } else if (left == 2) {
+        use_tile<DT, D>(t, count, a, body);
+        use_tile<DT, D>(t + 1, count, b, body);
+    } else if (left == 1) {
+        use_tile<DT, D>(t, count, a, body);
     }
-    if (t < ntiles) use_tile<DT, D>(t, count, a, body);
-    if (t + 1 < ntiles) use_tile<DT, D>(t + 1, count, b, body);
-    if (t + 2 < ntiles) use_tile<DT, D>(t + 2, count, c, body);
 }
 
 // Loads the first two tiles of a stream (clamped like every other tile).
@@ -269,6 +264,20 @@ __device__ __forceinline__ void for_rows(int count, RowOf row_of, Fetch fetch, B
     uint4 a[kUnroll], b[kUnroll];
     load_first2<DT, D>(count, row_of, fetch, a, b);
     for_rows_pre2<DT, D>(count, row_of, fetch, body, a, b);
+}
+
+// Streams elements [0, count) from LDS one 16-byte chunk per lane at a time
+// (LDS latency is short, and the registers stay free for the global row tiles
+// in flight).
+template <int DT, int D, typename RowOf, typename Fetch, typename Body>
+__device__ __forceinline__ void for_rows_lds(int count, RowOf row_of, Fetch fetch, Body body) {
+    using S = Shape<DT, D>;
+    const int cl = lane_id() % S::LPR;
+    const int span = ((count + S::GROUPS - 1) / S::GROUPS) * S::GROUPS;  // whole row groups
+    for (int e = wave_id() * S::RPW + lane_id() / S::LPR; e < span; e += S::GROUPS) {
+        const bool valid = e < count;
+        body(e, valid, fetch(row_of(valid ? e : count - 1), cl));
+    }
 }
 
 // x + (x of lane ^ 8, 16 or 32): each lane pair ends with the same bits.
@@ -663,24 +672,79 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     uint32_t *mvl = evl + p.evict_cap;
     unsigned char *stash = lds + p.off_stash;
 
-    const int ul = blockIdx.x;
-    const int sl = ul / (p.num_layers * p.num_kv_heads);
-    const int layer = (ul / p.num_kv_heads) % p.num_layers;
-    const int head = ul % p.num_kv_heads;
+    const int head = blockIdx.x, layer = blockIdx.y, sl = blockIdx.z;
+    const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
     const int64_t u = (int64_t)p.unit0 + ul;
-    const int n = p.n[sl], N = p.N[sl];
+    const int n = p.nN[2 * sl], N = p.nN[2 * sl + 1];
     const int64_t off = (int64_t)sl * p.s_seq + (int64_t)layer * p.s_layer + (int64_t)head * p.s_head;
     const char *vb = p.v + off;
-    const int64_t ss = p.s_slot;
+    const uint32_t ss32 = p.s_slot;
     const int64_t cap = p.capacity;
     const int lane = lane_id();
     const int cl = lane % S::LPR;
 
-    const bool score_mode = p.mode == kModeScore;
-    double *st = score_mode ? nullptr : (p.running_sum ? p.running_sum + u * (D + 1) : nullptr);
+    // Every argument needed before the first row load is fetched here, in one
+    // batch of scalar loads (the empty asm keeps the compiler from spreading
+    // the loads over the branches below, one round trip each).
+    double *const arg_rs = p.running_sum;
+    float *const arg_scores = p.scores;
+    uint8_t *const arg_keep = p.keep;
+    const int arg_mode = p.mode, arg_stash = p.stash_rows;
+    asm volatile("" ::"s"(arg_rs), "s"(arg_scores), "s"(arg_keep), "s"(arg_mode), "s"(arg_stash), "s"(n),
+                 "s"(N), "s"(vb), "s"(ss32));
+    const bool score_mode = arg_mode == kModeScore;
+    double *st = arg_rs ? arg_rs + u * (D + 1) : nullptr;  // null in kModeScore
     const bool evict = !score_mode && n > N;
-    float *scores_out = p.scores ? p.scores + u * cap : nullptr;
-    uint8_t *keep_out = p.keep ? p.keep + u * cap : nullptr;
+    float *scores_out = arg_scores ? arg_scores + u * cap : nullptr;
+    uint8_t *keep_out = arg_keep ? arg_keep + u * cap : nullptr;
+
+    const bool need_scores = score_mode || evict || scores_out;
+
+    // The rows are read in one software-pipelined stream of tiles over two
+    // parts: first the rows not yet in the running sum, [count, n), which give
+    // the mean (staged in LDS when they fit), then the rows still to be
+    // scored: [0, count) when the first part was staged, all of [0, n)
+    // otherwise.  The state's token count and column sums are read first.  The
+    // first two tiles go out right behind them for the steady-state guess
+    // count = min(N, n) and go out again only if the guess was wrong, so that
+    // either way exactly two tiles are in flight, in the same order, and every
+    // wait counts exactly.  Nothing branches before these loads (a unit with
+    // no rows reads row 0 of its slab and ignores it): the kernel arguments
+    // arrive in one batch and the row tiles go out right behind them.
+    const double *stp = st ? st : reinterpret_cast<const double *>(vb);
+    const double craw = stp[st ? D : 0];
+    const double st_col = stp[st ? min((int)threadIdx.x, D) : 0];
+    const int lastrow = max(n - 1, 0);
+    struct Plan {
+        int cnt, fresh, tiles_f, second, tiles;  // second: rows of the scoring part
+    };
+    auto plan_for = [&](int cnt) {
+        Plan q;
+        q.cnt = cnt;
+        q.fresh = n - cnt;
+        q.tiles_f = (q.fresh + S::STEP - 1) / S::STEP;
+        q.second = !need_scores ? 0 : (q.fresh <= arg_stash ? cnt : n);
+        q.tiles = q.tiles_f + (q.second + S::STEP - 1) / S::STEP;
+        return q;
+    };
+    // chunk k of tile t of the stream; a tile past the end reads the last row
+    // (never used)
+    auto load_chunk = [&](const Plan &q, int t, int k) -> uint4 {
+        const bool first = t < q.tiles_f;
+        const int lim = first ? q.fresh : q.second;
+        const int rbase = first ? q.cnt : 0;
+        const int e = (first ? t : t - q.tiles_f) * S::STEP + (k * NW + wave_id()) * S::RPW + lane / S::LPR;
+        const int r = (t < q.tiles && lim > 0) ? rbase + min(e, lim - 1) : lastrow;
+        return load_stream(vb, row_off(r, ss32, cl));
+    };
+    auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kUnroll]) {
+#pragma unroll
+        for (int k = 0; k < kUnroll; ++k) buf[k] = load_chunk(q, t, k);
+    };
+    const Plan guessed = plan_for(st ? min(N, n) : 0);
+    uint4 ta[kUnroll], tb[kUnroll];
+    load_v(guessed, 0, ta);
+    load_v(guessed, 1, tb);
 
     if (n <= 0) {
         if (st) {
@@ -688,47 +752,33 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         }
         return;
     }
-    const bool need_scores = score_mode || evict || scores_out;
     if (!need_scores && !st) {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
         return;
-    }
-
-    // The state's token count says which rows are new: [count, n).  It is read
-    // first; in steady state it equals N, so the loads of rows [min(N, n), n)
-    // go out right behind it instead of waiting for it (path A below uses them
-    // only if the guess holds).  Every load here is unconditional, so each later
-    // wait counts exactly.
-    const double craw = *(st ? st + D : reinterpret_cast<const double *>(vb));
-    const int guess = min(N, n);
-    const bool spec = st && guess > 0 && n - guess > 0 && n - guess <= 2 * S::STEP;
-    uint4 new_a[kUnroll], new_b[kUnroll];
-    {
-        const int gb = spec ? guess : n - 1;   // otherwise one row, read and not used
-        auto guess_row = [&](int e) { return min(gb + e, n - 1); };
-        load_first2<DT, D>(spec ? n - guess : 1, guess_row,
-                           [&](int r, int c) { return load_stream(vb + (int64_t)r * ss + c * 16); },
-                           new_a, new_b);
     }
     // one early read of the unit's K slab warms its address translation before
     // the gather moves K rows; the value is only looked at after scoring
     uint32_t kprobe = 0u;
     if (evict && p.k && threadIdx.x == 0)
-        kprobe = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss));
+        kprobe = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss32));
     int count = 0;
     if (st) count = (craw >= 0.0 && craw <= (double)n && craw == (double)(int)craw) ? (int)craw : 0;
-    const int fresh = n - count;
-    const bool stashed = fresh <= p.stash_rows;
-    auto gfetch = [&](int r, int c) -> uint4 { return load_stream(vb + (int64_t)r * ss + c * 16); };
+    const Plan q = count == guessed.cnt ? guessed : plan_for(count);
+    if (count != guessed.cnt) {
+        load_v(q, 0, ta);
+        load_v(q, 1, tb);
+    }
+    const int fresh = q.fresh;
+    const bool stashed = fresh <= arg_stash;
     auto sfetch = [&](int r, int c) -> uint4 {
         return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
     };
-    const int lastrow = n - 1;
     auto fresh_row = [&](int e) { return min(count + e, lastrow); };
-    auto old_row = [&](int e) { return min(e, lastrow); };
-    const bool score_old = need_scores && count > 0;
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
-    const bool to_lds = evict;  // keys of every evicting unit go to LDS
+    // keys go to LDS for the selection and for the score output: no global
+    // store sits between the row loads of the stream (a store in flight makes
+    // every later load wait for all outstanding memory operations)
+    const bool to_lds = evict || scores_out;
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
     float m[S::EPL];                          // this lane's columns of v_bar (Dir: v_bar / |v_bar|)
     bool mean_zero = false;
@@ -748,8 +798,10 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     };
     auto finish_mean = [&]() {
         block_col_sums<DT, D>(acc, red, H.sum);
-        for (int t = threadIdx.x; t < D; t += NT) {
-            const double old_sum = count > 0 ? st[t] : 0.0;
+        static_assert(D <= NT, "one thread per column");
+        if (threadIdx.x < D) {
+            const int t = threadIdx.x;
+            const double old_sum = count > 0 ? st_col : 0.0;
             const double s = old_sum + H.sum[t];
             H.old_sum[t] = old_sum;
             H.sum[t] = s;
@@ -817,35 +869,57 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
             }
-            if (scores_out) scores_out[r] = s;
         }
     };
 
     auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
-    if (score_old && spec && count == guess) {
-        // path A: the new block fits two tiles and was loaded above (every CU's
-        // new rows reach the memory controllers ahead of any old-row traffic);
-        // the first two tiles of the old rows go out as soon as it has landed,
-        // to arrive while the mean is reduced
-        uint4 pre_a[kUnroll], pre_b[kUnroll];
-        use_tile<DT, D>(0, fresh, new_a, mean_body);
-        use_tile<DT, D>(1, fresh, new_b, mean_body);
-        __builtin_amdgcn_sched_barrier(0);
-        load_first2<DT, D>(count, old_row, gfetch, pre_a, pre_b);
-        __builtin_amdgcn_sched_barrier(0);
+    // once the first part is summed: the mean, then the staged rows' scores
+    auto switch_parts = [&]() {
         finish_mean();
-        // the staged new rows are scored from LDS while the old-row tiles are in flight
-        if (stashed) for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
-        for_rows_pre2<DT, D>(count, old_row, gfetch, on_row, pre_a, pre_b);
-        if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
-    } else {
-        for_rows<DT, D>(fresh, fresh_row, gfetch, mean_body);
-        finish_mean();
-        if (need_scores) {
-            if (stashed) for_rows<DT, D>(fresh, fresh_row, sfetch, on_fresh);
-            if (score_old) for_rows<DT, D>(count, old_row, gfetch, on_row);
-            if (!stashed) for_rows<DT, D>(fresh, fresh_row, gfetch, on_fresh);
+        if (stashed && need_scores) for_rows_lds<DT, D>(fresh, fresh_row, sfetch, on_fresh);
+    };
+    // Tile t is used chunk by chunk, and when tile tn is to follow in the same
+    // registers, chunk k of tn is requested as soon as chunk k of t is used:
+    // the row loads in flight never drop below two tiles less one chunk.
+    auto use_load_v = [&](int t, uint4 (&buf)[kUnroll], int tn) {
+        if (t == q.tiles_f) switch_parts();
+        const int eb = wave_id() * S::RPW + lane / S::LPR;
+        if (t < q.tiles_f) {
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int e = t * S::STEP + k * NW * S::RPW + eb;
+                mean_body(e, e < fresh, buf[k]);
+                if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int e = (t - q.tiles_f) * S::STEP + k * NW * S::RPW + eb;
+                on_row(e, e < q.second, buf[k]);
+                if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+            }
         }
+    };
+    {
+        const int T = q.tiles;
+        int t = 0;
+        for (; t + 3 < T; t += 2) {
+            use_load_v(t, ta, t + 2);
+            use_load_v(t + 1, tb, t + 3);
+        }
+        // the last one to three tiles: no load past the end
+        const int left = T - t;
+        if (left == 3) {
+            use_load_v(t, ta, t + 2);
+            use_load_v(t + 1, tb, -1);
+            use_load_v(t + 2, ta, -1);
+        } else if (left == 2) {
+            use_load_v(t, ta, -1);
+            use_load_v(t + 1, tb, -1);
+        } else if (left == 1) {
+            use_load_v(t, ta, -1);
+        }
+        if (T <= q.tiles_f) switch_parts();  // the stream had no scoring part
     }
     // the probe value is consumed only here (the empty asm keeps the compiler
     // from testing it, and so waiting for it, next to the load)
@@ -862,6 +936,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (threadIdx.x < 4) H.bc[100 + threadIdx.x] = 0u;  // candidate count, keep mask
     }
     __syncthreads();
+    if (scores_out)  // the key is the score's bits with the sign bit set
+        for (int j = threadIdx.x; j < n; j += NT) scores_out[j] = __uint_as_float(keys[j] & 0x7FFFFFFFu);
     if (score_mode) return;
 
     // ---- select (Sec. 2.1, Eq. eviction) ----
@@ -914,7 +990,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
         const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
         auto vfetch = [&](int r) -> uint4 {
-            return (stashed && r >= count) ? sfetch(r, cl) : load_stream(vb + (int64_t)r * ss + cl * 16);
+            return (stashed && r >= count) ? sfetch(r, cl) : load_stream(vb, row_off(r, ss32, cl));
         };
         double acc[S::EPL];
 #pragma unroll
@@ -947,17 +1023,17 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 // ignored) so that no use can be hoisted next to its load.
 #pragma unroll
                 for (int k = 0; k < KV; ++k)
-                    km[k] = load_stream(ksrc + (int64_t)src[k] * ss + cl * 16);
+                    km[k] = load_stream(ksrc, row_off(src[k], ss32, cl));
                 if constexpr (!STASH) {
 #pragma unroll
-                    for (int k = 0; k < KV; ++k) vm[k] = load_stream(vb + (int64_t)src[k] * ss + cl * 16);
+                    for (int k = 0; k < KV; ++k) vm[k] = load_stream(vb, row_off(src[k], ss32, cl));
                 }
                 if (pos) {
 #pragma unroll
                     for (int k = 0; k < KV; ++k) ps[k] = pos[src[k]];
                 }
 #pragma unroll
-                for (int k = 0; k < KV; ++k) vh[k] = load_stream(vb + (int64_t)dst[k] * ss + cl * 16);
+                for (int k = 0; k < KV; ++k) vh[k] = load_stream(vb, row_off(dst[k], ss32, cl));
                 if constexpr (STASH) {
 #pragma unroll
                     for (int k = 0; k < KV; ++k) vm[k] = sfetch(src[k], cl);
@@ -967,8 +1043,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 for (int k = 0; k < KV; ++k) {
                     const int e = e0 + k * S::GROUPS + g;
                     if (e >= n_moves) continue;
-                    if (kb) store_stream(kb + (int64_t)dst[k] * ss + cl * 16, km[k]);
-                    store_stream(vw + (int64_t)dst[k] * ss + cl * 16, vm[k]);
+                    if (kb) store_stream(kb, row_off(dst[k], ss32, cl), km[k]);
+                    store_stream(vw, row_off(dst[k], ss32, cl), vm[k]);
                     if (pos && cl == 0) pos[dst[k]] = ps[k];
                 }
                 if (st) {  // new sum = old - holes + movers
@@ -1015,7 +1091,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                     vh[k] = vfetch((int)evl[ec]);
                     if (ec < n_moves) {
                         const int src = (int)mvl[ec];
-                        km[k] = kb ? load_stream(kb + (int64_t)src * ss + cl * 16) : make_uint4(0u, 0u, 0u, 0u);
+                        km[k] = kb ? load_stream(kb, row_off(src, ss32, cl)) : make_uint4(0u, 0u, 0u, 0u);
                         vm[k] = vfetch(src);
                     }
                 }
@@ -1030,8 +1106,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                     if (e < n_moves) {
                         const int dst = (int)evl[e];
                         const int src = (int)mvl[e];
-                        if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, km[k]);
-                        store_stream(vw + (int64_t)dst * ss + cl * 16, vm[k]);
+                        if (kb) store_stream(kb, row_off(dst, ss32, cl), km[k]);
+                        store_stream(vw, row_off(dst, ss32, cl), vm[k]);
                         if (pos && cl == 0) pos[dst] = pos[src];
                     }
                 }
@@ -1054,10 +1130,10 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
     extern __shared__ __align__(16) unsigned char lds[];
     LdsHead &H = *reinterpret_cast<LdsHead *>(lds);
     uint32_t *keys = reinterpret_cast<uint32_t *>(lds + p.off_keys);
-    const int ul = blockIdx.x;
-    const int sl = ul / (p.num_layers * p.num_kv_heads);
+    const int sl = blockIdx.z;
+    const int ul = (sl * p.num_layers + blockIdx.y) * p.num_kv_heads + blockIdx.x;
     const int64_t u = (int64_t)p.unit0 + ul;
-    const int n = p.n[sl], N = p.N[sl];
+    const int n = p.nN[2 * sl], N = p.nN[2 * sl + 1];
     const int64_t cap = p.capacity;
     const float *sc = p.scores_in + u * cap;
     uint8_t *keep = p.keep + u * cap;
@@ -1085,12 +1161,10 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     LdsHead &H = *reinterpret_cast<LdsHead *>(lds);
     uint32_t *holes = reinterpret_cast<uint32_t *>(lds + p.off_lists);
     uint32_t *movers = holes + p.evict_cap;
-    const int ul = blockIdx.x;
-    const int sl = ul / (p.num_layers * p.num_kv_heads);
-    const int layer = (ul / p.num_kv_heads) % p.num_layers;
-    const int head = ul % p.num_kv_heads;
+    const int head = blockIdx.x, layer = blockIdx.y, sl = blockIdx.z;
+    const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
     const int64_t u = (int64_t)p.unit0 + ul;
-    const int n = p.n[sl], N = p.N[sl];
+    const int n = p.nN[2 * sl], N = p.nN[2 * sl + 1];
     if (n <= N) return;
     const int64_t cap = p.capacity;
     const uint8_t *keep = p.keep_in + u * cap;
@@ -1138,16 +1212,16 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     char *kb = p.k ? p.k + off : nullptr;
     char *vb = p.v + off;
     int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
-    const int64_t ss = p.s_slot;
+    const uint32_t ss32 = p.s_slot;
     const int cl = lane % S::LPR;
     const int g = wave_id() * S::RPW + lane / S::LPR;
     for (int e = g; e < moves; e += S::GROUPS) {
         const int dst = (int)holes[e];
         const int src = (int)movers[e];
-        const uint4 kv = kb ? load_stream(kb + (int64_t)src * ss + cl * 16) : make_uint4(0u, 0u, 0u, 0u);
-        const uint4 vv = load_stream(vb + (int64_t)src * ss + cl * 16);
-        if (kb) store_stream(kb + (int64_t)dst * ss + cl * 16, kv);
-        store_stream(vb + (int64_t)dst * ss + cl * 16, vv);
+        const uint4 kv = kb ? load_stream(kb, row_off(src, ss32, cl)) : make_uint4(0u, 0u, 0u, 0u);
+        const uint4 vv = load_stream(vb, row_off(src, ss32, cl));
+        if (kb) store_stream(kb, row_off(dst, ss32, cl), kv);
+        store_stream(vb, row_off(dst, ss32, cl), vv);
         if (pos && cl == 0) pos[dst] = pos[src];
     }
 }
@@ -1179,31 +1253,32 @@ template <int DT> void *compact_kernel_for(int head_dim) {
     return nullptr;
 }
 
-hipError_t launch(void *fn, int num_units, size_t lds_bytes, hipStream_t stream,
+hipError_t launch(void *fn, int num_seqs, size_t lds_bytes, hipStream_t stream,
                   const UnitParams &p) {
     if (!fn) return hipErrorInvalidDeviceFunction;
     void *args[] = {const_cast<UnitParams *>(&p)};
-    return hipLaunchKernel(fn, dim3(num_units), dim3(NT), args, lds_bytes, stream);
+    const dim3 grid(p.num_kv_heads, p.num_layers, num_seqs);
+    return hipLaunchKernel(fn, grid, dim3(NT), args, lds_bytes, stream);
 }
 
 }  // namespace
 
-hipError_t launch_step(const UnitParams &p, int num_units, int dtype, int head_dim,
+hipError_t launch_step(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                        int variant, size_t lds_bytes, hipStream_t stream) {
     void *fn = dtype == 0 ? step_kernel_for<0>(head_dim, variant)
                           : step_kernel_for<1>(head_dim, variant);
-    return launch(fn, num_units, lds_bytes, stream, p);
+    return launch(fn, num_seqs, lds_bytes, stream, p);
 }
 
-hipError_t launch_select(const UnitParams &p, int num_units, size_t lds_bytes,
+hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
                          hipStream_t stream) {
-    return launch(reinterpret_cast<void *>(&select_kernel), num_units, lds_bytes, stream, p);
+    return launch(reinterpret_cast<void *>(&select_kernel), num_seqs, lds_bytes, stream, p);
 }
 
-hipError_t launch_compact(const UnitParams &p, int num_units, int dtype, int head_dim,
+hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream) {
     void *fn = dtype == 0 ? compact_kernel_for<0>(head_dim) : compact_kernel_for<1>(head_dim);
-    return launch(fn, num_units, lds_bytes, stream, p);
+    return launch(fn, num_seqs, lds_bytes, stream, p);
 }
 
 }  // namespace vd

@@ -30,22 +30,20 @@ struct LdsHead {
 };
 static_assert(sizeof(LdsHead) % 16 == 0, "LDS head must keep 16-byte alignment");
 
+// Kernel arguments.  The fields every workgroup needs before its first row
+// load come first, so that one batch of scalar loads fetches them; the unit's
+// (sequence, layer, head) is the workgroup's (z, y, x) position in the grid.
 struct UnitParams {
     char *k;                  // first unit of the launch's first sequence; may be null
     char *v;
-    int64_t s_seq, s_layer, s_head, s_slot;   // strides in BYTES
+    double *running_sum;      // [U][D+1] or null
+    int64_t s_seq, s_layer, s_head;   // strides in BYTES
+    uint32_t s_slot;          // bytes from one slot to the next (a slab spans < 4 GiB)
     int32_t num_layers, num_kv_heads;
     int32_t unit0;            // global index of the launch's first unit
     int32_t capacity;
     int32_t mode;             // Mode
-    int32_t pad0;
-    double *running_sum;      // [U][D+1] or null
-    int32_t *pos;             // [U][capacity] or null
-    float *scores;            // [U][capacity] or null (required in kModeScore)
-    const float *scores_in;   // select kernel input
-    uint8_t *keep;            // [U][capacity] or null (output of step/select)
-    const uint8_t *keep_in;   // compact kernel input
-    float *mean_out;          // [U][D] or null
+    int32_t stash_rows;       // rows the stash holds
     // dynamic LDS layout (byte offsets from the start of dynamic LDS)
     int32_t off_keys;         // keys / fp64 reduction scratch
     int32_t off_lists;        // evicted (or hole) list, then mover list
@@ -53,17 +51,22 @@ struct UnitParams {
     int32_t keys_cap;         // entries in the keys region
     int32_t evict_cap;        // entries of the first list
     int32_t move_cap;         // entries of the second list
-    int32_t stash_rows;       // rows the stash holds
-    int32_t pad1;
-    int32_t n[kMaxSeqsPerLaunch];
-    int32_t N[kMaxSeqsPerLaunch];
+    int32_t pad0;
+    int32_t *pos;             // [U][capacity] or null
+    float *scores;            // [U][capacity] or null (required in kModeScore)
+    const float *scores_in;   // select kernel input
+    uint8_t *keep;            // [U][capacity] or null (output of step/select)
+    const uint8_t *keep_in;   // compact kernel input
+    float *mean_out;          // [U][D] or null
+    int32_t nN[2 * kMaxSeqsPerLaunch];   // n and N of each sequence of the launch, interleaved
 };
 
-hipError_t launch_step(const UnitParams &p, int num_units, int dtype, int head_dim,
+// Each launches one workgroup per unit of `num_seqs` sequences.
+hipError_t launch_step(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                        int variant, size_t lds_bytes, hipStream_t stream);
-hipError_t launch_select(const UnitParams &p, int num_units, size_t lds_bytes,
+hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
                          hipStream_t stream);
-hipError_t launch_compact(const UnitParams &p, int num_units, int dtype, int head_dim,
+hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream);
 
 }  // namespace vd
