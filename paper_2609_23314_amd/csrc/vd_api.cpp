@@ -95,8 +95,11 @@ vd_status plan_step_lds(const vd_cache_desc *d, UnitParams &p, int ns, bool scor
             want_rows = std::max(want_rows, n);
         }
     }
+    // keys, then (when the unit selects) the second histogram buffer; the fp64
+    // reduction scratch aliases the region
     const int64_t red_bytes = int64_t(vd::kWaves) * d->head_dim * 8;
-    const int64_t keys_bytes = align16(std::max<int64_t>(int64_t(keys_cap) * 4, red_bytes));
+    const int64_t sel_bytes = keys_cap > 0 ? align16(int64_t(keys_cap) * 4) + int64_t(vd::kBins) * 4 : 0;
+    const int64_t keys_bytes = align16(std::max<int64_t>(sel_bytes, red_bytes));
     const int64_t lists_bytes = align16(int64_t(evict_cap + move_cap) * 4);
     const int64_t used = int64_t(sizeof(vd::LdsHead)) + keys_bytes + lists_bytes;
     if (used > vd::kLdsBytes) return VD_ERR_UNSUPPORTED;
@@ -157,7 +160,7 @@ vd_status vd_select_topn(const vd_cache_desc *desc, const float *scores, const i
         for (int i = 0; i < ns; ++i) nmax = std::max(nmax, p.nN[2 * i]);
         p.off_keys = int32_t(sizeof(vd::LdsHead));
         p.keys_cap = nmax;
-        const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(nmax) * 4));
+        const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(nmax) * 4)) + size_t(vd::kBins) * 4;
         if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
         st = launched(vd::launch_select(p, ns, lds, reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;

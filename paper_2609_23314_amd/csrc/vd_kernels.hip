@@ -330,234 +330,67 @@ __device__ __forceinline__ void block_col_sums(double *acc, double *red, double 
 
 // ---------------------------------------------------------------- selection
 
-struct Threshold {
-    uint32_t key;      // key of the N-th largest score
-    int need;          // how many keys equal to `key` are kept (the lowest slots)
-    int count_eq;      // how many keys equal `key`
-};
+// The wave index as a scalar (the compiler cannot prove threadIdx.x / 64
+// uniform, and per-wave loops and offsets would otherwise run on vector
+// registers under exec masks).
+__device__ __forceinline__ int wave_id_s() { return __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); }
 
-// The N-th largest of keys[0..n) (1 <= N < n).  Each pass histograms the keys
-// still in play, bin = (key - lo) >> shift with shift chosen so that the range
-// [lo, hi] fills at most kBins bins, and keeps the bin holding the N-th
-// largest; once a bin holds at most kCand keys, one wave ranks them by
-// (key desc, slot asc).  A pass narrows the range 512-fold or more, so at most
-// four passes run.
-// kmin / kmax are this thread's partial minimum and maximum of the keys.
-__device__ __forceinline__ Threshold select_threshold(const uint32_t *keys, int n, int N, uint32_t kmin,
-                                      uint32_t kmax, LdsHead &H) {
-    kmin = wave_min_u32(kmin);
-    kmax = wave_max_u32(kmax);
-    if (lane_id() == 0) {
-        H.bc[wave_id()] = kmin;
-        H.bc[32 + wave_id()] = kmax;
-    }
-    __syncthreads();
-    uint32_t lo = H.bc[0], hi = H.bc[32];
-#pragma unroll
-    for (int i = 1; i < NW; ++i) {
-        lo = min(lo, H.bc[i]);
-        hi = max(hi, H.bc[32 + i]);
-    }
-    __syncthreads();
-    int need = N;
-    int in_range = n;
-    for (;;) {
-        if (lo == hi) return Threshold{lo, need, in_range};
-        const int bits = 32 - __clz(hi - lo);   // bits of the largest offset
-        const int shift = bits > 10 ? bits - 10 : 0;
-        H.hist[threadIdx.x] = 0u;  // NT == kBins
-        if (threadIdx.x == 0) H.bc[100] = 0u;
-        __syncthreads();
-        for (int j = threadIdx.x; j < n; j += NT) {
-            const uint32_t k = keys[j];
-            if (k >= lo && k <= hi) atomicAdd(&H.hist[(k - lo) >> shift], 1u);
-        }
-        __syncthreads();
-        // thread t owns bin kBins-1-t, so a prefix sum in thread order counts
-        // the keys in higher bins
-        const uint32_t bin = kBins - 1 - threadIdx.x;
-        const uint32_t h = H.hist[bin];
-        const uint32_t incl = wave_incl_scan(h);
-        if (lane_id() == 63) H.bc[wave_id()] = incl;  // wave totals
-        __syncthreads();
-        uint32_t above = incl - h;
-        for (int i = 0; i < wave_id(); ++i) above += H.bc[i];
-        const uint32_t un = (uint32_t)need;
-        if (above < un && un <= above + h) {
-            H.bc[64] = bin;
-            H.bc[65] = above;
-            H.bc[66] = h;
-        }
-        __syncthreads();
-        const uint64_t b = H.bc[64];
-        need -= (int)H.bc[65];
-        in_range = (int)H.bc[66];
-        const uint64_t top = (uint64_t)lo + ((b + 1) << shift) - 1u;
-        hi = top < (uint64_t)hi ? (uint32_t)top : hi;
-        lo = lo + (uint32_t)(b << shift);
-        if (lo == hi || in_range > kCand) {
-            __syncthreads();
-            continue;
-        }
-        // few keys left: gather them and rank them exactly
-        for (int j = threadIdx.x; j < n; j += NT) {
-            const uint32_t k = keys[j];
-            if (k >= lo && k <= hi) {
-                const uint32_t slot = atomicAdd(&H.bc[100], 1u);
-                H.cand_key[slot] = k;
-                H.cand_idx[slot] = (uint32_t)j;
-            }
-        }
-        __syncthreads();
-        {
-            // lane t holds candidate t; wave w ranks candidates w, w+16, w+32, w+48
-            // by counting, with one ballot, the candidates that order before each
-            const int c = in_range;
-            const int t = lane_id();
-            const bool live = t < c;
-            const uint32_t kt = live ? H.cand_key[t] : 0u;
-            const uint32_t jt = live ? H.cand_idx[t] : 0u;
-            for (int i = wave_id(); i < c; i += NW) {
-                const uint32_t ki = lane_u32(kt, i), ji = lane_u32(jt, i);
-                const uint32_t rank =
-                    __popcll(__ballot(live && (kt > ki || (kt == ki && jt < ji))));
-                if (rank == (uint32_t)(need - 1)) {  // the candidate that fixes the threshold
-                    const uint32_t n_gt = __popcll(__ballot(live && kt > ki));
-                    const uint32_t n_eq = __popcll(__ballot(live && kt == ki));
-                    if (t == 0) {
-                        H.bc[67] = ki;
-                        H.bc[68] = (uint32_t)need - n_gt;
-                        H.bc[69] = n_eq;
-                    }
-                }
-            }
-        }
-        __syncthreads();
-        const Threshold th{H.bc[67], (int)H.bc[68], (int)H.bc[69]};
-        __syncthreads();
-        return th;
-    }
+// Number of set bits of a ballot mask in the lanes below this one.
+__device__ __forceinline__ uint32_t ballot_rank(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
-// Decides keep(j) for j < n from the threshold and appends the evicted slots
-// (ascending) to evl and the kept slots >= N (ascending) to mvl; writes
-// keep_out if given.  Wave w owns a contiguous segment of slots, so only the
-// per-wave counts cross waves.  Returns the number of movers.
-__device__ __forceinline__ int build_lists(const uint32_t *keys, int n, int N, const Threshold &th,
-                           uint32_t *evl, int evict_cap, uint32_t *mvl, int move_cap,
-                           uint8_t *keep_out, LdsHead &H) {
-    const int w = wave_id(), lane = lane_id();
-    const int seg = (((n + NW - 1) / NW) + 63) & ~63;
+// Sum of x over lanes 0..i-1 (i uniform, 0 <= i <= 16) of a value held by lanes 0..15.
+__device__ __forceinline__ uint32_t sum_below16(uint32_t x, int i) {
+    const uint32_t incl = wave_incl_scan(x);
+    return i > 0 ? lane_u32(incl, i - 1) : 0u;
+}
+
+// Threshold and lists for the fused pass.  The kept set is the first N
+// elements in (key desc, slot asc) order; with (T, J) the N-th of them,
+// keep(j) <=> key_j > T or (key_j == T and j <= J).
+//
+// Before the barrier that ended scoring every wave has stored its key minimum
+// in bc[w] and maximum in bc[16 + w], and hist[] and the candidate counter
+// bc[100] are zero; hist2[] (kBins entries, just past the keys) is
+// scratch.  Wave w owns the slot segment [w*seg, (w+1)*seg).
+// Histogram passes over the key range narrow it to one bin (the two histogram
+// buffers alternate, so a pass costs two barriers).  Once the bin holds at
+// most kCand keys, one sweep gathers them and publishes every wave's counts of
+// the sure evictions (below the bin) and sure movers (above it); the waves
+// rank the candidates between them to find (T, J), after which every wave
+// knows the decision on every candidate and hence its own list offsets
+// without a further count.  If the bin holds more than kCand keys they are
+// all equal and J is found by counting equal keys in slot order.  evl
+// receives every evicted slot and mvl every kept slot >= N, both ascending (so
+// evl starts with the holes below N); keep_out is written if given.  Returns
+// the number of movers.
+__device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
+                                                uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H,
+                                                uint32_t *hist2) {
+    const int w = wave_id_s(), lane = lane_id();
+    const int seg = (((n + NW - 1) / NW) + 63) & ~63;  // slots per wave, whole blocks
     const int j0 = w * seg;
     const int j1 = min(n, j0 + seg);
-    const bool rank_eq = th.count_eq != th.need;
-    const uint32_t T = th.key;
-    uint32_t eq_before = 0;
-    if (rank_eq) {
-        uint32_t c = 0;
-        for (int jb = j0; jb < j1; jb += 64) {
-            const int j = jb + lane;
-            c += __popcll(__ballot(j < j1 && keys[j] == T));
-        }
-        if (lane == 0) H.bc[w] = c;
-        __syncthreads();
-        for (int i = 0; i < w; ++i) eq_before += H.bc[i];
-        __syncthreads();
-    }
-    auto decide = [&](int j, bool valid, uint32_t &eqr) -> bool {
-        const uint32_t k = valid ? keys[j] : 0u;
-        const bool gt = valid && k > T;
-        const bool eq = valid && k == T;
-        if (!rank_eq) return gt || eq;
-        const uint64_t m = __ballot(eq);
-        const uint32_t r = eqr + __popcll(m & lanes_below());
-        eqr += __popcll(m);
-        return gt || (eq && r < (uint32_t)th.need);
-    };
-    uint32_t cev = 0, cmv = 0, eqr = eq_before;
-    for (int jb = j0; jb < j1; jb += 64) {
-        const int j = jb + lane;
-        const bool valid = j < j1;
-        const bool keep = decide(j, valid, eqr);
-        cev += __popcll(__ballot(valid && !keep));
-        cmv += __popcll(__ballot(valid && keep && j >= N));
-    }
-    if (lane == 0) {
-        H.bc[32 + w] = cev;
-        H.bc[64 + w] = cmv;
-    }
-    __syncthreads();
-    uint32_t ev_off = 0, mv_off = 0, mv_tot = 0;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-        const uint32_t e = H.bc[32 + i], m = H.bc[64 + i];
-        ev_off += i < w ? e : 0u;
-        mv_off += i < w ? m : 0u;
-        mv_tot += m;
-    }
-    eqr = eq_before;
-    for (int jb = j0; jb < j1; jb += 64) {
-        const int j = jb + lane;
-        const bool valid = j < j1;
-        const bool keep = decide(j, valid, eqr);
-        const bool ev = valid && !keep;
-        const bool mv = valid && keep && j >= N;
-        const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
-        const uint32_t rev = ev_off + __popcll(mev & lanes_below());
-        const uint32_t rmv = mv_off + __popcll(mmv & lanes_below());
-        if (ev && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
-        if (mv && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
-        if (keep_out && valid) keep_out[j] = keep ? 1 : 0;
-        ev_off += __popcll(mev);
-        mv_off += __popcll(mmv);
-    }
-    __syncthreads();
-    return (int)mv_tot;
-}
-
-// Threshold and lists for the fused pass, with five block barriers on the
-// usual path.  Before the barrier that ends scoring, every wave has stored its
-// key minimum in bc[w] and maximum in bc[16 + w], and the histogram, the
-// candidate counter bc[100] and the keep mask bc[102..103] are zero.  Each
-// histogram pass is scanned by every wave on its own (the bin holding the N-th
-// largest key is found without a further barrier); once that bin holds at
-// most kCand keys, one sweep over the wave's slot segment counts the sure
-// decisions (below / above the bin) and collects the bin's keys, the waves
-// rank those candidates by (key desc, slot asc) between them, and each wave
-// writes its part of the lists.  Many equal keys at the
-// threshold (more than kCand) fall back to build_lists, which ranks them by
-// slot.  Lists and keep_out as in build_lists; returns the number of movers.
-__device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
-                                uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H) {
-    const int w = wave_id(), lane = lane_id();
-    uint32_t lo = H.bc[0], hi = H.bc[16];
-#pragma unroll
-    for (int i = 1; i < NW; ++i) {
-        lo = min(lo, H.bc[i]);
-        hi = max(hi, H.bc[16 + i]);
-    }
-    int need = N;
-    int in_range = n;
-    for (int pass = 0; in_range > kCand; ++pass) {
-        if (lo == hi) {  // more than kCand equal keys hold the threshold
-            __syncthreads();  // bc[0..31] has been read by every wave; build_lists reuses bc
-            return build_lists(keys, n, N, Threshold{lo, need, in_range}, evl, evict_cap, mvl,
-                               move_cap, keep_out, H);
-        }
-        if (pass > 0) {  // every wave has read the previous histogram
-            __syncthreads();
-            H.hist[threadIdx.x] = 0u;  // NT == kBins
-            __syncthreads();
-        }
+    uint32_t lo = wave_min_u32(lane < NW ? H.bc[lane] : 0xFFFFFFFFu);
+    uint32_t hi = wave_max_u32(lane < NW ? H.bc[16 + lane] : 0u);
+    int need = N;       // 1-based rank of (T, J) among the keys in [lo, hi]
+    int in_range = n;   // keys in [lo, hi]
+    for (int pass = 0; in_range > kCand && lo != hi; ++pass) {
+        uint32_t *hc = (pass & 1) ? hist2 : H.hist;
+        uint32_t *hn = (pass & 1) ? H.hist : hist2;
         const int bits = 32 - __clz(hi - lo);  // bits of the largest offset
         const int shift = bits > 10 ? bits - 10 : 0;
-        for (int j = threadIdx.x; j < n; j += NT) {
-            const uint32_t k = keys[j];
-            if (k >= lo && k <= hi) atomicAdd(&H.hist[(k - lo) >> shift], 1u);
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            const uint32_t k = j < j1 ? keys[j] : 0u;
+            if (j < j1 && k >= lo && k <= hi) atomicAdd(&hc[(k - lo) >> shift], 1u);
         }
         __syncthreads();
-        // wave w owns bins kBins-1-64w .. kBins-64-64w (descending keys)
-        const uint32_t total = wave_incl_scan(H.hist[kBins - 1 - threadIdx.x]);
+        // wave w owns bins kBins-1-64w .. kBins-64-64w (descending keys); the
+        // other buffer was last read before the barrier above
+        const uint32_t total = wave_incl_scan(hc[kBins - 1 - threadIdx.x]);
+        hn[threadIdx.x] = 0u;  // NT == kBins
         if (lane == 63) H.bc[80 + w] = total;
         __syncthreads();
         const uint32_t un = (uint32_t)need;
@@ -566,7 +399,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         // the wave holding it (the totals sum to in_range >= need, so one lane qualifies)
         const int tw = max(__ffsll(__ballot(lane < NW && wincl >= un)) - 1, 0);
         const uint32_t before = lane_u32(wincl - wt, tw);
-        const uint32_t hb = H.hist[kBins - 1 - (tw * 64 + lane)];
+        const uint32_t hb = hc[kBins - 1 - (tw * 64 + lane)];
         const uint32_t bincl = wave_incl_scan(hb) + before;
         const int tl = max(__ffsll(__ballot(bincl >= un)) - 1, 0);
         const uint32_t h = lane_u32(hb, tl);
@@ -578,81 +411,128 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         hi = top < (uint64_t)hi ? (uint32_t)top : hi;
         lo = lo + (uint32_t)(b << shift);
     }
-    // one sweep: sure evictions (below lo), sure movers (above hi, slot >= N),
-    // and the candidates in [lo, hi]
-    const int seg = (((n + NW - 1) / NW) + 63) & ~63;
-    const int j0 = w * seg;
-    const int j1 = min(n, j0 + seg);
-    uint32_t c_lo = 0, c_mv = 0;
-    for (int jb = j0; jb < j1; jb += 64) {
-        const int j = jb + lane;
-        const bool valid = j < j1;
-        const uint32_t k = valid ? keys[j] : 0u;
-        const bool below = valid && k < lo;
-        const bool over = valid && k > hi;
-        c_lo += __popcll(__ballot(below));
-        c_mv += __popcll(__ballot(over && j >= N));
-        if (valid && !below && !over) {
-            const uint32_t slot = atomicAdd(&H.bc[100], 1u);
-            if (slot < (uint32_t)kCand) {  // the bin holds exactly in_range <= kCand keys
-                H.cand_key[slot] = k;
-                H.cand_idx[slot] = (uint32_t)j;
+    uint32_t T, J, ev_off, mv_off, mv_tot;
+    if (in_range <= kCand) {
+        // gather the keys in [lo, hi] and publish this wave's sure evictions
+        // (below lo) and sure movers (above hi)
+        uint32_t sev = 0u, smv = 0u;
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            const bool v = j < j1;
+            const uint32_t k = v ? keys[j] : 0u;
+            const bool c = v && k >= lo && k <= hi;
+            sev += __popcll(__ballot(v && k < lo));
+            smv += __popcll(__ballot(v && k > hi && j >= N));
+            const uint64_t m = __ballot(c);
+            if (m) {
+                uint32_t base = 0u;
+                if (lane == 0) base = atomicAdd(&H.bc[100], (uint32_t)__popcll(m));
+                base = __builtin_amdgcn_readfirstlane(base);
+                const uint32_t slot = base + ballot_rank(m);
+                if (c && slot < (uint32_t)kCand) {  // the bin holds exactly in_range <= kCand keys
+                    H.cand_key[slot] = k;
+                    H.cand_idx[slot] = (uint32_t)j;
+                }
             }
         }
+        if (lane == 0) {
+            H.bc[32 + w] = sev;
+            H.bc[48 + w] = smv;
+        }
+        __syncthreads();
+        // lane t holds candidate t; wave w ranks candidates w, w+16, w+32, w+48
+        const int cnt = in_range;
+        const bool live = lane < cnt;
+        const uint32_t ck = live ? H.cand_key[lane] : 0u;
+        const uint32_t ci = live ? H.cand_idx[lane] : 0u;
+        for (int i = w; i < cnt; i += NW) {
+            const uint32_t ki = lane_u32(ck, i), ji = lane_u32(ci, i);
+            const uint32_t rank = __popcll(__ballot(live && (ck > ki || (ck == ki && ci < ji))));
+            if (rank == (uint32_t)(need - 1)) {
+                if (lane == 0) {
+                    H.bc[67] = ki;
+                    H.bc[68] = ji;
+                }
+            }
+        }
+        const uint32_t se = lane < NW ? H.bc[32 + lane] : 0u;
+        const uint32_t sm = lane < NW ? H.bc[48 + lane] : 0u;
+        __syncthreads();
+        T = H.bc[67];
+        J = H.bc[68];
+        // list offsets: the sure counts of the waves before this one, plus the
+        // candidates in their segments that go (evicted) or move
+        const bool ckeep = live && (ck > T || (ck == T && ci <= J));
+        const bool cbefore = live && (int)ci < j0;
+        ev_off = sum_below16(se, w) + (uint32_t)__popcll(__ballot(cbefore && !ckeep));
+        mv_off = sum_below16(sm, w) + (uint32_t)__popcll(__ballot(cbefore && ckeep && (int)ci >= N));
+        mv_tot = sum_below16(sm, NW) + (uint32_t)__popcll(__ballot(ckeep && (int)ci >= N));
+    } else {
+        // every key in [lo, hi] equals T = lo: J is the slot of the need-th of
+        // them in slot order
+        T = lo;
+        uint32_t ce = 0u;
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            ce += __popcll(__ballot(j < j1 && keys[j] == T));
+        }
+        if (lane == 0) H.bc[32 + w] = ce;
+        __syncthreads();
+        const uint32_t eq_before = sum_below16(lane < NW ? H.bc[32 + lane] : 0u, w);
+        if (eq_before < (uint32_t)need && (uint32_t)need <= eq_before + ce) {
+            uint32_t r = eq_before;
+            for (int jb = j0; jb < j1; jb += 64) {
+                const int j = jb + lane;
+                const uint64_t m = __ballot(j < j1 && keys[j] == T);
+                const uint32_t c = (uint32_t)__popcll(m);
+                if (r + c >= (uint32_t)need) {  // the (need - r)-th set lane of m
+                    uint64_t mm = m;
+                    for (uint32_t q = 1; q < (uint32_t)need - r; ++q) mm &= mm - 1;
+                    if (lane == 0) H.bc[68] = (uint32_t)(jb + __ffsll((unsigned long long)mm) - 1);
+                    break;
+                }
+                r += c;
+            }
+        }
+        __syncthreads();
+        J = H.bc[68];
+        // counts per wave, then offsets
+        uint32_t cev = 0u, cmv = 0u;
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            const bool v = j < j1;
+            const uint32_t k = v ? keys[j] : 0u;
+            const bool keep = v && (k > T || (k == T && (uint32_t)j <= J));
+            cev += __popcll(__ballot(v && !keep));
+            cmv += __popcll(__ballot(keep && j >= N));
+        }
+        if (lane == 0) {
+            H.bc[32 + w] = cev;  // every wave has read bc[32..47] before the barrier above
+            H.bc[48 + w] = cmv;
+        }
+        __syncthreads();
+        const uint32_t e_i = lane < NW ? H.bc[32 + lane] : 0u;
+        const uint32_t m_i = lane < NW ? H.bc[48 + lane] : 0u;
+        ev_off = sum_below16(e_i, w);
+        mv_off = sum_below16(m_i, w);
+        mv_tot = sum_below16(m_i, NW);
     }
-    if (lane == 0) {
-        H.bc[32 + w] = c_lo;
-        H.bc[48 + w] = c_mv;
-    }
-    __syncthreads();
-    // lane t holds candidate t; wave w ranks candidates w, w+16, w+32, w+48 with
-    // one ballot each and records the kept ones in the mask bc[102..103]
-    const int c = in_range;
-    const bool live = lane < c;
-    const uint32_t ck = live ? H.cand_key[lane] : 0u;
-    const uint32_t ci = live ? H.cand_idx[lane] : 0u;
-    for (int i = w; i < c; i += NW) {
-        const uint32_t ki = lane_u32(ck, i), ji = lane_u32(ci, i);
-        const uint32_t rank = __popcll(__ballot(live && (ck > ki || (ck == ki && ci < ji))));
-        if (lane == 0 && rank < (uint32_t)need) atomicOr(&H.bc[102 + (i >> 5)], 1u << (i & 31));
-    }
-    __syncthreads();
-    const uint64_t keep_mask = ((uint64_t)H.bc[103] << 32) | H.bc[102];
-    const bool ckeep = (keep_mask >> lane) & 1ull;
-    const uint32_t mine_lo = (uint32_t)j0;  // candidates of earlier segments have smaller slots
-    uint32_t ev_off = __popcll(__ballot(live && !ckeep && ci < mine_lo));
-    uint32_t mv_off = __popcll(__ballot(live && ckeep && ci >= (uint32_t)N && ci < mine_lo));
-    uint32_t mv_tot = __popcll(__ballot(ckeep && ci >= (uint32_t)N));
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-        const uint32_t e = H.bc[32 + i], m = H.bc[48 + i];
-        ev_off += i < w ? e : 0u;
-        mv_off += i < w ? m : 0u;
-        mv_tot += m;
-    }
+    // each wave writes its part of the lists
     for (int jb = j0; jb < j1; jb += 64) {
         const int j = jb + lane;
-        const bool valid = j < j1;
-        const uint32_t k = valid ? keys[j] : 0u;
-        bool keep = valid && k > hi;
-        uint64_t mi = __ballot(valid && k >= lo && k <= hi);
-        while (mi) {  // slots in the bin take their candidate's decision
-            const int bl = __ffsll((unsigned long long)mi) - 1;
-            mi &= mi - 1;
-            const uint32_t jj = lane_u32((uint32_t)j, bl);
-            const int t = __ffsll(__ballot(live && ci == jj)) - 1;  // its candidate lane
-            if (lane == bl) keep = t >= 0 && ((keep_mask >> t) & 1ull);
-        }
-        const bool ev = valid && !keep;
-        const bool mv = valid && keep && j >= N;
+        const bool v = j < j1;
+        const uint32_t k = v ? keys[j] : 0u;
+        const bool keep = v && (k > T || (k == T && (uint32_t)j <= J));
+        const bool ev = v && !keep;
+        const bool mv = keep && j >= N;
         const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
-        const uint32_t rev = ev_off + __popcll(mev & lanes_below());
-        const uint32_t rmv = mv_off + __popcll(mmv & lanes_below());
+        const uint32_t rev = ev_off + ballot_rank(mev);
+        const uint32_t rmv = mv_off + ballot_rank(mmv);
         if (ev && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
         if (mv && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
-        if (keep_out && valid) keep_out[j] = keep ? 1 : 0;
-        ev_off += __popcll(mev);
-        mv_off += __popcll(mmv);
+        if (keep_out && v) keep_out[j] = keep ? 1 : 0;
+        ev_off += (uint32_t)__popcll(mev);
+        mv_off += (uint32_t)__popcll(mmv);
     }
     __syncthreads();
     return (int)mv_tot;
@@ -933,7 +813,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             H.bc[16 + wave_id()] = kmax;
         }
         H.hist[threadIdx.x] = 0u;  // NT == kBins
-        if (threadIdx.x < 4) H.bc[100 + threadIdx.x] = 0u;  // candidate count, keep mask
+        if (threadIdx.x == 0) H.bc[100] = 0u;  // candidate count
     }
     __syncthreads();
     if (scores_out)  // the key is the score's bits with the sign bit set
@@ -972,7 +852,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = j == victim ? 0 : 1;
             __syncthreads();
         } else {
-            n_moves = select_and_build(keys, n, N, evl, p.evict_cap, mvl, p.move_cap, keep_out, H);
+            n_moves = select_and_build(keys, n, N, evl, p.evict_cap, mvl, p.move_cap, keep_out, H,
+                                       keys + ((n + 3) & ~3));
         }
     } else {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
@@ -1148,9 +1029,16 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
         kmin = min(kmin, k);
         kmax = max(kmax, k);
     }
+    kmin = wave_min_u32(kmin);
+    kmax = wave_max_u32(kmax);
+    if (lane_id() == 0) {
+        H.bc[wave_id()] = kmin;
+        H.bc[16 + wave_id()] = kmax;
+    }
+    H.hist[threadIdx.x] = 0u;  // NT == kBins
+    if (threadIdx.x == 0) H.bc[100] = 0u;
     __syncthreads();
-    const Threshold th = select_threshold(keys, n, N, kmin, kmax, H);
-    build_lists(keys, n, N, th, nullptr, 0, nullptr, 0, keep, H);
+    select_and_build(keys, n, N, nullptr, 0, nullptr, 0, keep, H, keys + ((n + 3) & ~3));
 }
 
 // Standalone gather from a keep mask.

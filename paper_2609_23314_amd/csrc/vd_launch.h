@@ -45,7 +45,7 @@ struct UnitParams {
     int32_t mode;             // Mode
     int32_t stash_rows;       // rows the stash holds
     // dynamic LDS layout (byte offsets from the start of dynamic LDS)
-    int32_t off_keys;         // keys / fp64 reduction scratch
+    int32_t off_keys;         // keys, then the second histogram buffer / fp64 reduction scratch
     int32_t off_lists;        // evicted (or hole) list, then mover list
     int32_t off_stash;        // staged rows
     int32_t keys_cap;         // entries in the keys region
