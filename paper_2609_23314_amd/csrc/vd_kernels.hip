@@ -93,6 +93,32 @@ template <int LPR> __device__ __forceinline__ float row_sum(float x) {
     return x;
 }
 
+// Sums of four rows at once: a[q] is this lane's partial sum of row q (chunk
+// q of a tile), and each row spans the LPR lanes of one row group.  Two
+// exchanges inside each quad leave every lane with a pair sum of one row,
+// which is then summed over the lanes holding the same row; afterwards lane c
+// of the group holds the full sum of row quad_row(c).  Five adds for four
+// rows, against four per row one at a time.
+__device__ __forceinline__ int quad_row(int c) { return ((c & 1) << 1) | ((c >> 1) & 1); }
+template <int LPR> __device__ __forceinline__ float row_sums4(const float (&a)[4], int c) {
+    const bool b0 = c & 1, b1 = (c >> 1) & 1;
+    // lanes with bit 0 clear keep rows 0 and 1, the others rows 2 and 3
+    const float k0 = b0 ? a[2] : a[0], k1 = b0 ? a[3] : a[1];
+    const float g0 = b0 ? a[0] : a[2], g1 = b0 ? a[1] : a[3];
+    const float p0 = k0 + dpp<0xB1>(g0);  // quad_perm [1,0,3,2]: lane ^ 1
+    const float p1 = k1 + dpp<0xB1>(g1);
+    // lanes with bit 1 clear keep the first of the two, the others the second
+    float x = (b1 ? p1 : p0) + dpp<0x4E>(b1 ? p0 : p1);  // quad_perm [2,3,0,1]: lane ^ 2
+    if constexpr (LPR == 8) x += __shfl_xor(x, 4);
+    if constexpr (LPR >= 16) {
+        x += dpp<0x124>(x);  // row_ror:4
+        x += dpp<0x128>(x);  // row_ror:8
+    }
+    if constexpr (LPR >= 32) x += __shfl_xor(x, 16);
+    if constexpr (LPR >= 64) x += __shfl_xor(x, 32);
+    return x;
+}
+
 template <int CTRL, int ROW_MASK = 0xF>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
     return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, ROW_MASK, 0xF, false);
@@ -264,20 +290,6 @@ __device__ __forceinline__ void for_rows(int count, RowOf row_of, Fetch fetch, B
     uint4 a[kUnroll], b[kUnroll];
     load_first2<DT, D>(count, row_of, fetch, a, b);
     for_rows_pre2<DT, D>(count, row_of, fetch, body, a, b);
-}
-
-// Streams elements [0, count) from LDS one 16-byte chunk per lane at a time
-// (LDS latency is short, and the registers stay free for the global row tiles
-// in flight).
-template <int DT, int D, typename RowOf, typename Fetch, typename Body>
-__device__ __forceinline__ void for_rows_lds(int count, RowOf row_of, Fetch fetch, Body body) {
-    using S = Shape<DT, D>;
-    const int cl = lane_id() % S::LPR;
-    const int span = ((count + S::GROUPS - 1) / S::GROUPS) * S::GROUPS;  // whole row groups
-    for (int e = wave_id() * S::RPW + lane_id() / S::LPR; e < span; e += S::GROUPS) {
-        const bool valid = e < count;
-        body(e, valid, fetch(row_of(valid ? e : count - 1), cl));
-    }
 }
 
 // x + (x of lane ^ 8, 16 or 32): each lane pair ends with the same bits.
@@ -598,7 +610,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     struct Plan {
         int cnt, fresh, tiles_f, second, tiles;  // second: rows of the scoring part
     };
-    auto plan_for = [&](int cnt) {
+    auto plan_for = [&](int cnt) __attribute__((always_inline)) {
         Plan q;
         q.cnt = cnt;
         q.fresh = n - cnt;
@@ -609,7 +621,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     };
     // chunk k of tile t of the stream; a tile past the end reads the last row
     // (never used)
-    auto load_chunk = [&](const Plan &q, int t, int k) -> uint4 {
+    auto load_chunk = [&](const Plan &q, int t, int k) __attribute__((always_inline)) -> uint4 {
         const bool first = t < q.tiles_f;
         const int lim = first ? q.fresh : q.second;
         const int rbase = first ? q.cnt : 0;
@@ -617,7 +629,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         const int r = (t < q.tiles && lim > 0) ? rbase + min(e, lim - 1) : lastrow;
         return load_stream(vb, row_off(r, ss32, cl));
     };
-    auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kUnroll]) {
+    auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kUnroll]) __attribute__((always_inline)) {
 #pragma unroll
         for (int k = 0; k < kUnroll; ++k) buf[k] = load_chunk(q, t, k);
     };
@@ -650,10 +662,10 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     }
     const int fresh = q.fresh;
     const bool stashed = fresh <= arg_stash;
-    auto sfetch = [&](int r, int c) -> uint4 {
+    auto sfetch = [&](int r, int c) __attribute__((always_inline)) -> uint4 {
         return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
     };
-    auto fresh_row = [&](int e) { return min(count + e, lastrow); };
+    auto fresh_row = [&](int e) __attribute__((always_inline)) { return min(count + e, lastrow); };
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
     // keys go to LDS for the selection and for the score output: no global
     // store sits between the row loads of the stream (a store in flight makes
@@ -667,7 +679,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     double acc[S::EPL];
 #pragma unroll
     for (int i = 0; i < S::EPL; ++i) acc[i] = 0.0;
-    auto mean_body = [&](int e, bool valid, uint4 w) {
+    auto mean_body = [&](int e, bool valid, uint4 w) __attribute__((always_inline)) {
         float x[S::EPL];
         E::unpack(w, x);
         if (valid) {
@@ -676,7 +688,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             if (stashed) *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
         }
     };
-    auto finish_mean = [&]() {
+    auto finish_mean = [&]() __attribute__((always_inline)) {
         block_col_sums<DT, D>(acc, red, H.sum);
         static_assert(D <= NT, "one thread per column");
         if (threadIdx.x < D) {
@@ -702,14 +714,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             for (int t = threadIdx.x; t < D; t += NT) H.udir[t] = mean_zero ? 0.f : H.mean[t] / mn;
             __syncthreads();
         }
-        if (score_mode && p.mean_out)
-            for (int t = threadIdx.x; t < D; t += NT) p.mean_out[u * D + t] = H.mean[t];
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) m[i] = (VAR == 1 ? H.udir : H.mean)[cl * S::EPL + i];
     };
 
     // ---- scores (Sec. 3.2) ----
-    auto on_row = [&](int r, bool valid, uint4 w) {
+    auto on_row = [&](int r, bool valid, uint4 w) __attribute__((always_inline)) {
         float x[S::EPL];
         E::unpack(w, x);
         float s;
@@ -752,16 +762,65 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         }
     };
 
-    auto on_fresh = [&](int e, bool valid, uint4 w) { on_row(count + e, valid, w); };
-    // once the first part is summed: the mean, then the staged rows' scores
-    auto switch_parts = [&]() {
-        finish_mean();
-        if (stashed && need_scores) for_rows_lds<DT, D>(fresh, fresh_row, sfetch, on_fresh);
+    auto on_fresh = [&](int e, bool valid, uint4 w) __attribute__((always_inline)) { on_row(count + e, valid, w); };
+    // L2 and Norm score the four chunks of a tile together (one square root per
+    // lane, one key store per row); chunk k of the tile holds element
+    // e0 + k*NW*RPW of this lane's row group, valid below lim, at row rbase + e
+    constexpr bool kBatch = VAR != 1 && kUnroll == 4;
+    auto partial = [&](uint4 w) __attribute__((always_inline)) {
+        float x[S::EPL];
+        E::unpack(w, x);
+        float a = 0.f;
+#pragma unroll
+        for (int i = 0; i < S::EPL; ++i) {
+            const float t = VAR == 0 ? x[i] - m[i] : x[i];
+            a = fmaf(t, t, a);
+        }
+        return a;
     };
+    auto score4 = [&](const float (&a)[4], int e0, int lim, int rbase) __attribute__((always_inline)) {
+        const float s = score_sqrt(row_sums4<S::LPR>(a, cl));
+        const int e = e0 + quad_row(cl) * NW * S::RPW;
+        if (cl < 4 && e < lim) {
+            const uint32_t key = score_key(s);
+            if (to_lds) {
+                keys[rbase + e] = key;
+                kmin = min(kmin, key);
+                kmax = max(kmax, key);
+            }
+        }
+    };
+    // staged tile i (rows count + [i*STEP, (i+1)*STEP)) scored from LDS
+    auto score_stash_tile = [&](int i) __attribute__((always_inline)) {
+        const int e0 = i * S::STEP + wave_id() * S::RPW + lane / S::LPR;
+        if constexpr (kBatch) {
+            uint4 w4[kUnroll];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) w4[k] = sfetch(fresh_row(e0 + k * NW * S::RPW), cl);
+            float a[4];
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) a[k] = partial(w4[k]);
+            score4(a, e0, fresh, count);
+        } else {
+#pragma unroll
+            for (int k = 0; k < kUnroll; ++k) {
+                const int e = e0 + k * NW * S::RPW;
+                on_fresh(e, e < fresh, sfetch(fresh_row(e), cl));
+            }
+        }
+    };
+    const bool score_stash = stashed && need_scores;
+    const int stash_tiles = score_stash ? q.tiles_f : 0;
     // Tile t is used chunk by chunk, and when tile tn is to follow in the same
     // registers, chunk k of tn is requested as soon as chunk k of t is used:
     // the row loads in flight never drop below two tiles less one chunk.
-    auto use_load_v = [&](int t, uint4 (&buf)[kUnroll], int tn) {
+    // once the first part is summed: the mean, then the staged rows' scores
+    // (the first two scoring tiles are in flight meanwhile)
+    auto switch_parts = [&]() __attribute__((always_inline)) {
+        finish_mean();
+        for (int i = 0; i < stash_tiles; ++i) score_stash_tile(i);
+    };
+    auto use_load_v = [&](int t, uint4 (&buf)[kUnroll], int tn) __attribute__((always_inline)) {
         if (t == q.tiles_f) switch_parts();
         const int eb = wave_id() * S::RPW + lane / S::LPR;
         if (t < q.tiles_f) {
@@ -772,11 +831,22 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 if (tn >= 0) buf[k] = load_chunk(q, tn, k);
             }
         } else {
+            const int ts = t - q.tiles_f;
+            if constexpr (kBatch) {
+                float a[4];
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
-                const int e = (t - q.tiles_f) * S::STEP + k * NW * S::RPW + eb;
-                on_row(e, e < q.second, buf[k]);
-                if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+                for (int k = 0; k < kUnroll; ++k) {
+                    a[k] = partial(buf[k]);
+                    if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+                }
+                score4(a, ts * S::STEP + eb, q.second, 0);
+            } else {
+#pragma unroll
+                for (int k = 0; k < kUnroll; ++k) {
+                    const int e = ts * S::STEP + k * NW * S::RPW + eb;
+                    on_row(e, e < q.second, buf[k]);
+                    if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+                }
             }
         }
     };
@@ -818,7 +888,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     __syncthreads();
     if (scores_out)  // the key is the score's bits with the sign bit set
         for (int j = threadIdx.x; j < n; j += NT) scores_out[j] = __uint_as_float(keys[j] & 0x7FFFFFFFu);
-    if (score_mode) return;
+    if (score_mode) {  // the mean leaves after the stream, like the scores
+        if (p.mean_out)
+            for (int t = threadIdx.x; t < D; t += NT) p.mean_out[u * D + t] = H.mean[t];
+        return;
+    }
 
     // ---- select (Sec. 2.1, Eq. eviction) ----
     int n_moves = 0;
@@ -870,7 +944,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         char *vw = p.v + off;
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
         const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
-        auto vfetch = [&](int r) -> uint4 {
+        auto vfetch = [&](int r) __attribute__((always_inline)) -> uint4 {
             return (stashed && r >= count) ? sfetch(r, cl) : load_stream(vb, row_off(r, ss32, cl));
         };
         double acc[S::EPL];
@@ -883,7 +957,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             // the stores, with no load waiting behind another.
             const char *ksrc = kb ? kb : vb;  // without K a V row stands in, unused
             const int wrow = wave_id() * S::RPW;
-            auto batch = [&](int e0, auto kvc, auto stashc) {
+            auto batch = [&](int e0, auto kvc, auto stashc) __attribute__((always_inline)) {
                 constexpr int KV = decltype(kvc)::value;
                 constexpr bool STASH = decltype(stashc)::value;
                 int dst[KV], src[KV];

@@ -1,0 +1,62 @@
+"""Code generation of the HIP kernels for gfx950, checked on the host.
+
+The kernels keep every LDS access on the LDS instructions and everything
+else in registers: a lambda the compiler does not inline turns the captured
+LDS pointers into generic ones (flat accesses through a stack frame in
+scratch), which both slows the pass and turns an LDS access beyond the
+allocation, harmless for an LDS instruction, into a memory fault.  This test
+compiles the device code to assembly and rejects calls, flat accesses and
+stack frames beyond a few register spills.
+"""
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2609_23314_amd import build as lib_build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2609_23314_amd", "csrc")
+MAX_PRIVATE_BYTES = 64   # per lane: register spills only
+
+
+@pytest.fixture(scope="module")
+def kernels(tmp_path_factory):
+    out = tmp_path_factory.mktemp("asm") / "vd_kernels.s"
+    cmd = [lib_build.hipcc(), f"--offload-arch={lib_build.ARCH}", "--cuda-device-only", "-S",
+           "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           *lib_build.DEVICE_FLAGS, os.path.join(CSRC, "vd_kernels.hip"), "-o", str(out)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    text = out.read_text()
+    # split into functions: "name:" label lines that open a function body
+    bodies = {}
+    for m in re.finditer(r"^(_Z\S+):\s*;\s*@", text, flags=re.M):
+        start = m.end()
+        end = text.find(".end_amdhsa_kernel", start)
+        nxt = text.find("\n_Z", start)
+        stop = min(x for x in (end, nxt, len(text)) if x >= 0)
+        bodies[m.group(1)] = (text[start:stop], text[stop:text.find("\n", end) if end >= 0 else stop])
+    sizes = dict(re.findall(r"\.amdhsa_kernel (\S+)\n(?:.*\n)*?\s*\.amdhsa_private_segment_fixed_size (\d+)",
+                            text))
+    return text, bodies, {k: int(v) for k, v in sizes.items()}
+
+
+def test_every_kernel_is_a_single_function(kernels):
+    text, bodies, _ = kernels
+    assert "s_swappc" not in text, "a device function was called instead of inlined"
+    names = list(bodies)
+    assert names and all("kernel" in n for n in names), names
+
+
+def test_no_flat_memory_access(kernels):
+    text, _, _ = kernels
+    flat = re.findall(r"^\s*(flat_\w+)", text, flags=re.M)
+    assert not flat, f"generic-pointer accesses in the kernels: {sorted(set(flat))}"
+
+
+def test_stack_frames_hold_spills_only(kernels):
+    _, _, sizes = kernels
+    assert sizes, "no kernel descriptors found"
+    big = {k: v for k, v in sizes.items() if v > MAX_PRIVATE_BYTES}
+    assert not big, big
