@@ -314,11 +314,11 @@ template <int O> __device__ __forceinline__ double xor_sum(double x) {
 }
 
 // Column sums of per-lane fp64 partials (each lane holds EPL columns of its
-// chunk) into out[0..D) in LDS; fixed reduction order.  `red` holds NW*D
-// doubles; `out` may be red itself (each thread reads and then writes only
-// its own column).
+// chunk), in a fixed order: thread t < D receives the total of column t (no
+// other thread receives anything).  `red` holds NW*D doubles; the caller
+// orders any later reuse of it with a barrier of its own.
 template <int DT, int D>
-__device__ __forceinline__ void block_col_sums(double *acc, double *red, double *out) {
+__device__ __forceinline__ double block_col_total(double *acc, double *red) {
     using S = Shape<DT, D>;
 #pragma unroll
     for (int i = 0; i < S::EPL; ++i) {
@@ -331,13 +331,13 @@ __device__ __forceinline__ void block_col_sums(double *acc, double *red, double 
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) red[w * D + lane * S::EPL + i] = acc[i];
     __syncthreads();
-    for (int t = threadIdx.x; t < D; t += NT) {
-        double s = 0.0;
+    static_assert(D <= NT, "one thread per column");
+    double s = 0.0;
+    if (threadIdx.x < D) {
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) s += red[ww * D + t];
-        out[t] = s;
+        for (int ww = 0; ww < NW; ++ww) s += red[ww * D + threadIdx.x];
     }
-    __syncthreads();
+    return s;
 }
 
 // ---------------------------------------------------------------- selection
@@ -689,12 +689,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         }
     };
     auto finish_mean = [&]() __attribute__((always_inline)) {
-        block_col_sums<DT, D>(acc, red, H.sum);
-        static_assert(D <= NT, "one thread per column");
+        const double fresh_sum = block_col_total<DT, D>(acc, red);
         if (threadIdx.x < D) {
             const int t = threadIdx.x;
             const double old_sum = count > 0 ? st_col : 0.0;
-            const double s = old_sum + H.sum[t];
+            const double s = old_sum + fresh_sum;
             H.old_sum[t] = old_sum;
             H.sum[t] = s;
             H.mean[t] = (float)(s / (double)n);
@@ -1069,9 +1068,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             }
         }
         if (st) {
-            block_col_sums<DT, D>(acc, red, red);  // red aliases keys, no longer needed
-            for (int t = threadIdx.x; t < D; t += NT)
-                st[t] = (steady ? H.old_sum[t] : H.sum[t]) + red[t];
+            const double delta = block_col_total<DT, D>(acc, red);  // red aliases keys, no longer needed
+            if (threadIdx.x < D) st[threadIdx.x] = (steady ? H.old_sum[threadIdx.x] : H.sum[threadIdx.x]) + delta;
             if (threadIdx.x == 0) st[D] = (double)N;
         }
     } else if (st) {
