@@ -122,6 +122,14 @@ def time_pool(w, states, steps, warmup, dev):
             wv.copy_(st[1])
             wr.copy_(st[2])
 
+    # The copies above leave up to a few hundred MB of dirty lines in L2 and
+    # the MALL; a read of a buffer larger than both evicts them before each
+    # timed segment, so that the passes do not pay for the copies' write-back.
+    flush_buf = torch.zeros(1 << 28, dtype=torch.float32, device=dev)   # 1 GiB
+
+    def flush():
+        flush_buf.sum()
+
     stream = torch.cuda.current_stream(dev)
     done = 0
     for i in range(warmup):
@@ -133,6 +141,7 @@ def time_pool(w, states, steps, warmup, dev):
     while done < steps:
         seg = min(pool_n, steps - done)
         refill(done, seg)
+        flush()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)

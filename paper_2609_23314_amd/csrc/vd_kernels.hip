@@ -28,6 +28,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "vd_launch.h"
 
 namespace vd {
@@ -39,6 +41,7 @@ template <bool V> struct BoolC { static constexpr bool value = V; };
 constexpr int NT = kBlock;
 constexpr int NW = kWaves;
 constexpr int kUnroll = 4;  // 16-byte loads per lane per tile (two tiles in flight)
+constexpr int kChunks = 2 * kUnroll;  // the pass kernel's row stream: one tile of 8 in flight
 static_assert(NT == kBins, "the selection gives every thread one histogram bin");
 
 // ---------------------------------------------------------------- elements
@@ -171,6 +174,20 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // scalar-base load or store with one offset register per lane.
 __device__ __forceinline__ uint32_t row_off(int r, uint32_t ss, int chunk) {
     return (uint32_t)r * ss + (uint32_t)chunk * 16u;
+}
+
+// Zero, produced by an empty asm that takes x: code using it cannot be
+// scheduled before x is computed.
+__device__ __forceinline__ uint32_t zero_after(float x) {
+    uint32_t z = 0u;
+    asm("" : "+v"(z) : "v"(x));
+    return z;
+}
+template <int N> __device__ __forceinline__ uint32_t zero_after(const double (&x)[N]) {
+    uint32_t z = 0u;
+#pragma unroll
+    for (int i = 0; i < N; ++i) asm("" : "+v"(z) : "v"(x[i]));
+    return z;
 }
 
 // 16-byte load that bypasses cache retention: the value rows stream through once.
@@ -607,6 +624,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     const double craw = stp[st ? D : 0];
     const double st_col = stp[st ? min((int)threadIdx.x, D) : 0];
     const int lastrow = max(n - 1, 0);
+    constexpr int kStep = S::GROUPS * kChunks;  // rows per tile of the stream
     struct Plan {
         int cnt, fresh, tiles_f, second, tiles;  // second: rows of the scoring part
     };
@@ -614,29 +632,28 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         Plan q;
         q.cnt = cnt;
         q.fresh = n - cnt;
-        q.tiles_f = (q.fresh + S::STEP - 1) / S::STEP;
+        q.tiles_f = (q.fresh + kStep - 1) / kStep;
         q.second = !need_scores ? 0 : (q.fresh <= arg_stash ? cnt : n);
-        q.tiles = q.tiles_f + (q.second + S::STEP - 1) / S::STEP;
+        q.tiles = q.tiles_f + (q.second + kStep - 1) / kStep;
         return q;
     };
     // chunk k of tile t of the stream; a tile past the end reads the last row
     // (never used)
-    auto load_chunk = [&](const Plan &q, int t, int k) __attribute__((always_inline)) -> uint4 {
+    auto load_chunk = [&](const Plan &q, int t, int k, uint32_t z = 0u) __attribute__((always_inline)) -> uint4 {
         const bool first = t < q.tiles_f;
         const int lim = first ? q.fresh : q.second;
         const int rbase = first ? q.cnt : 0;
-        const int e = (first ? t : t - q.tiles_f) * S::STEP + (k * NW + wave_id()) * S::RPW + lane / S::LPR;
+        const int e = (first ? t : t - q.tiles_f) * kStep + (k * NW + wave_id()) * S::RPW + lane / S::LPR;
         const int r = (t < q.tiles && lim > 0) ? rbase + min(e, lim - 1) : lastrow;
-        return load_stream(vb, row_off(r, ss32, cl));
+        return load_stream(vb, row_off(r, ss32, cl) + z);
     };
-    auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kUnroll]) __attribute__((always_inline)) {
+    auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kChunks]) __attribute__((always_inline)) {
 #pragma unroll
-        for (int k = 0; k < kUnroll; ++k) buf[k] = load_chunk(q, t, k);
+        for (int k = 0; k < kChunks; ++k) buf[k] = load_chunk(q, t, k);
     };
     const Plan guessed = plan_for(st ? min(N, n) : 0);
-    uint4 ta[kUnroll], tb[kUnroll];
-    load_v(guessed, 0, ta);
-    load_v(guessed, 1, tb);
+    uint4 buf[kChunks];
+    load_v(guessed, 0, buf);
 
     if (n <= 0) {
         if (st) {
@@ -657,8 +674,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     if (st) count = (craw >= 0.0 && craw <= (double)n && craw == (double)(int)craw) ? (int)craw : 0;
     const Plan q = count == guessed.cnt ? guessed : plan_for(count);
     if (count != guessed.cnt) {
-        load_v(q, 0, ta);
-        load_v(q, 1, tb);
+        load_v(q, 0, buf);
     }
     const int fresh = q.fresh;
     const bool stashed = fresh <= arg_stash;
@@ -718,7 +734,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     };
 
     // ---- scores (Sec. 3.2) ----
-    auto on_row = [&](int r, bool valid, uint4 w) __attribute__((always_inline)) {
+    auto on_row = [&](int r, bool valid, uint4 w) __attribute__((always_inline)) -> float {
         float x[S::EPL];
         E::unpack(w, x);
         float s;
@@ -759,13 +775,14 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 kmax = max(kmax, key);
             }
         }
+        return s;
     };
 
     auto on_fresh = [&](int e, bool valid, uint4 w) __attribute__((always_inline)) { on_row(count + e, valid, w); };
     // L2 and Norm score the four chunks of a tile together (one square root per
     // lane, one key store per row); chunk k of the tile holds element
     // e0 + k*NW*RPW of this lane's row group, valid below lim, at row rbase + e
-    constexpr bool kBatch = VAR != 1 && kUnroll == 4;
+    constexpr bool kBatch = VAR != 1 && kUnroll == 4 && kChunks % 4 == 0;
     auto partial = [&](uint4 w) __attribute__((always_inline)) {
         float x[S::EPL];
         E::unpack(w, x);
@@ -809,42 +826,65 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         }
     };
     const bool score_stash = stashed && need_scores;
-    const int stash_tiles = score_stash ? q.tiles_f : 0;
-    // Tile t is used chunk by chunk, and when tile tn is to follow in the same
-    // registers, chunk k of tn is requested as soon as chunk k of t is used:
-    // the row loads in flight never drop below two tiles less one chunk.
-    // once the first part is summed: the mean, then the staged rows' scores
-    // (the first two scoring tiles are in flight meanwhile)
+    const int stash_tiles = score_stash ? (fresh + S::STEP - 1) / S::STEP : 0;
+    // Tile t is used chunk by chunk, and chunk k of tile t + 1 is requested
+    // into the same registers as soon as chunk k of t is used: the row loads
+    // in flight never drop below one tile less one chunk, and the loads cross
+    // from the first part to the second unbroken (the first scoring tile is in
+    // flight while the mean is finished and the staged rows are scored).  The
+    // two parts run as two loops, so that the mean's fp64 partials are dead
+    // while the scoring part runs.
     auto switch_parts = [&]() __attribute__((always_inline)) {
         finish_mean();
         for (int i = 0; i < stash_tiles; ++i) score_stash_tile(i);
     };
-    auto use_load_v = [&](int t, uint4 (&buf)[kUnroll], int tn) __attribute__((always_inline)) {
-        if (t == q.tiles_f) switch_parts();
-        const int eb = wave_id() * S::RPW + lane / S::LPR;
-        if (t < q.tiles_f) {
+    const int eb = wave_id() * S::RPW + lane / S::LPR;
+    // chunk k of scoring tile tn < tiles (no clamping to other parts needed)
+    auto load_scored = [&](int tn, int k, uint32_t z) __attribute__((always_inline)) -> uint4 {
+        const int e = (tn - q.tiles_f) * kStep + k * NW * S::RPW + eb;
+        return load_stream(vb, row_off(min(e, q.second - 1), ss32, cl) + z);
+    };
+    // The load that refills a chunk's registers takes its address through a
+    // zero that the compiler sees as computed from the chunk's results, so it
+    // is issued after the chunk's last use (issued earlier, it would land in
+    // other registers, copied back at the loop's end, which waits for it),
+    // and no later work moves above it (the loads stay spread out, so that
+    // about one tile stays in flight).
+    auto use_fresh = [&](int t, auto more) __attribute__((always_inline)) {
 #pragma unroll
-            for (int k = 0; k < kUnroll; ++k) {
-                const int e = t * S::STEP + k * NW * S::RPW + eb;
-                mean_body(e, e < fresh, buf[k]);
-                if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+        for (int k = 0; k < kChunks; ++k) {
+            const int e = t * kStep + k * NW * S::RPW + eb;
+            mean_body(e, e < fresh, buf[k]);
+            if constexpr (more()) {
+                buf[k] = load_chunk(q, t + 1, k, zero_after(acc));
+                __builtin_amdgcn_sched_barrier(0);
             }
-        } else {
-            const int ts = t - q.tiles_f;
-            if constexpr (kBatch) {
+        }
+    };
+    auto use_scored = [&](int t, auto more) __attribute__((always_inline)) {
+        const int e0 = (t - q.tiles_f) * kStep + eb;
+        if constexpr (kBatch) {
+#pragma unroll
+            for (int h = 0; h < kChunks; h += 4) {
                 float a[4];
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) {
-                    a[k] = partial(buf[k]);
-                    if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+                for (int k = h; k < h + 4; ++k) {
+                    a[k - h] = partial(buf[k]);
+                    if constexpr (more()) {
+                        buf[k] = load_scored(t + 1, k, zero_after(a[k - h]));
+                        __builtin_amdgcn_sched_barrier(0);
+                    }
                 }
-                score4(a, ts * S::STEP + eb, q.second, 0);
-            } else {
+                score4(a, e0 + h * NW * S::RPW, q.second, 0);
+            }
+        } else {
 #pragma unroll
-                for (int k = 0; k < kUnroll; ++k) {
-                    const int e = ts * S::STEP + k * NW * S::RPW + eb;
-                    on_row(e, e < q.second, buf[k]);
-                    if (tn >= 0) buf[k] = load_chunk(q, tn, k);
+            for (int k = 0; k < kChunks; ++k) {
+                const int e = e0 + k * NW * S::RPW;
+                const float sc = on_row(e, e < q.second, buf[k]);
+                if constexpr (more()) {
+                    buf[k] = load_scored(t + 1, k, zero_after(sc));
+                    __builtin_amdgcn_sched_barrier(0);
                 }
             }
         }
@@ -852,23 +892,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     {
         const int T = q.tiles;
         int t = 0;
-        for (; t + 3 < T; t += 2) {
-            use_load_v(t, ta, t + 2);
-            use_load_v(t + 1, tb, t + 3);
-        }
-        // the last one to three tiles: no load past the end
-        const int left = T - t;
-        if (left == 3) {
-            use_load_v(t, ta, t + 2);
-            use_load_v(t + 1, tb, -1);
-            use_load_v(t + 2, ta, -1);
-        } else if (left == 2) {
-            use_load_v(t, ta, -1);
-            use_load_v(t + 1, tb, -1);
-        } else if (left == 1) {
-            use_load_v(t, ta, -1);
-        }
-        if (T <= q.tiles_f) switch_parts();  // the stream had no scoring part
+        for (; t < q.tiles_f && t + 1 < T; ++t) use_fresh(t, std::true_type{});
+        if (t < q.tiles_f) use_fresh(t++, std::false_type{});  // no scoring part follows
+        switch_parts();
+        for (; t + 1 < T; ++t) use_scored(t, std::true_type{});
+        if (t < T) use_scored(t, std::false_type{});  // the last tile: no load past the end
     }
     // the probe value is consumed only here (the empty asm keeps the compiler
     // from testing it, and so waiting for it, next to the load)
