@@ -163,6 +163,27 @@ def time_pool(w, states, steps, warmup, dev):
     return wall_s, gpu_ms, alg, scan
 
 
+def stream_read_gbps(dev, nbytes=2 << 30, reps=5):
+    """Read bandwidth of the library's plain streaming read (vd_stream_read)
+    over a 2 GiB buffer: the practical HBM read ceiling on this GPU, next to
+    the 8 TB/s peak.  Best of `reps` timed runs, in GB/s."""
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device=dev)
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    vd.vd_stream_read(buf, sink)
+    torch.cuda.synchronize()
+    best = float("inf")
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        vd.vd_stream_read(buf, sink)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1) / 1e3)
+    del buf
+    return nbytes / best / 1e9
+
+
 def decode_state(w: synth.Workload, dev):
     """A decode step of every sequence: N old tokens and one new token in the
     cache (n = N + 1), and the running sum of the N old rows."""
@@ -326,6 +347,9 @@ def main():
     scan_gbps = sum(scan) / kernel_s / 1e9
     log(f"bench: {passes_per_s:.1f} passes/s wall, {ms_launch * 1e3:.2f} us per launch (HIP events)")
     traffic = load_traffic(w.name)
+    evicting_units = sum(w.num_layers * w.num_kv_heads for s_ in range(w.num_seqs)
+                         if base_state[3][s_] > w.budget[s_])
+    stream_gbps = stream_read_gbps(dev)
     out = {
         "metric": METRIC,
         "value": round(passes_per_s, 2),
@@ -347,8 +371,11 @@ def main():
                    "block": w.block,
                    "prompt": max(w.prompt), "n": max(base_state[3]), "variant": "l2",
                    "running_sum": True, "parallelism": "single GPU"},
+        "head_passes_per_s": round(passes_per_s * evicting_units, 1),
         "kv_gbps_scanned": round(scan_gbps, 1),
         "kv_scan_frac_of_hbm_peak": round(scan_gbps / HBM_PEAK_GBPS, 4),
+        "stream_read_gbps": round(stream_gbps, 1),
+        "alg_frac_of_stream_read": round(alg_gbps / stream_gbps, 4),
         "roofline": {"bound": "hbm", "achieved": round(alg_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(alg_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),

@@ -152,6 +152,16 @@ size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);
 /* A static description of a status code. */
 const char *vd_status_string(vd_status status);
 
+/* Measurement aid, not part of the method: reads `bytes` bytes of device
+ * memory at `buf` once with the pass kernel's 16-byte streaming loads, over
+ * the whole GPU, so that a caller can time the practical HBM read ceiling next
+ * to the pass.  `buf` must be 16-byte aligned and `bytes` a multiple of 16;
+ * `sink` is a device uint32 written with a value derived from the data only
+ * when that value is a fixed unlikely constant (it keeps the loads from being
+ * dropped).  Returns VD_ERR_INVALID_ARG for a null or misaligned argument,
+ * VD_ERR_HIP if the launch fails. */
+vd_status vd_stream_read(const void *buf, size_t bytes, uint32_t *sink, vd_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -239,6 +239,13 @@ size_t vd_evict_step_workspace_size(const vd_cache_desc *desc) {
     return 0;
 }
 
+vd_status vd_stream_read(const void *buf, size_t bytes, uint32_t *sink, vd_stream stream) {
+    if (!buf || !sink || bytes == 0 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(buf) % 16 != 0)
+        return VD_ERR_INVALID_ARG;
+    return vd::launch_stream_read(buf, bytes / 16, sink, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
+               ? VD_OK : VD_ERR_HIP;
+}
+
 const char *vd_status_string(vd_status status) {
     switch (status) {
         case VD_OK: return "ok";

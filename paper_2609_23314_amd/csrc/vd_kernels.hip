@@ -1263,10 +1263,42 @@ hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
     return launch(reinterpret_cast<void *>(&select_kernel), num_seqs, lds_bytes, stream, p);
 }
 
+// Plain streaming read with the pass kernel's access pattern: each workgroup
+// walks one contiguous part of the buffer, every lane keeping eight 16-byte
+// loads in flight, and folds the data into one word, stored only if it equals
+// a fixed constant.
+constexpr int kReadGroups = 1024;
+__global__ void __launch_bounds__(256) stream_read_kernel(const u32x4 *buf, size_t n16, uint32_t *sink) {
+    constexpr int kIn = 8, kTile = kIn * 256;
+    const size_t per = (n16 + kReadGroups - 1) / kReadGroups;
+    const size_t b0 = (size_t)blockIdx.x * per;
+    const size_t b1 = b0 + per < n16 ? b0 + per : n16;
+    uint32_t x = 0u;
+    size_t i = b0;
+    for (; i + kTile <= b1; i += kTile) {
+        u32x4 w[kIn];
+#pragma unroll
+        for (int k = 0; k < kIn; ++k) w[k] = __builtin_nontemporal_load(buf + i + k * 256 + threadIdx.x);
+#pragma unroll
+        for (int k = 0; k < kIn; ++k) x ^= w[k].x ^ w[k].y ^ w[k].z ^ w[k].w;
+    }
+    for (size_t j = i + threadIdx.x; j < b1; j += 256) {
+        const u32x4 w = __builtin_nontemporal_load(buf + j);
+        x ^= w.x ^ w.y ^ w.z ^ w.w;
+    }
+    if (x == 0x9E3779B9u) sink[0] = x;
+}
+
 hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream) {
     void *fn = dtype == 0 ? compact_kernel_for<0>(head_dim) : compact_kernel_for<1>(head_dim);
     return launch(fn, num_seqs, lds_bytes, stream, p);
+}
+
+hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream) {
+    hipLaunchKernelGGL(stream_read_kernel, dim3(kReadGroups), dim3(256), 0, stream,
+                       reinterpret_cast<const u32x4 *>(buf), n16, sink);
+    return hipGetLastError();
 }
 
 }  // namespace vd

@@ -68,5 +68,7 @@ hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
                          hipStream_t stream);
 hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream);
+// Reads n16 16-byte words once over the whole GPU (a measurement aid).
+hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream);
 
 }  // namespace vd

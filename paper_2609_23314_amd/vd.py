@@ -24,7 +24,7 @@ VARIANTS = {"l2": 0, "dir": 1, "norm": 2}
 MAX_CAPACITY = 16384
 
 EXPORTS = ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step",
-           "vd_evict_step_workspace_size", "vd_status_string")
+           "vd_evict_step_workspace_size", "vd_status_string", "vd_stream_read")
 
 
 class VdError(RuntimeError):
@@ -69,6 +69,8 @@ def load():
     lib.vd_evict_step_workspace_size.restype = ctypes.c_size_t
     lib.vd_status_string.argtypes = [ctypes.c_int]
     lib.vd_status_string.restype = ctypes.c_char_p
+    lib.vd_stream_read.argtypes = [P, SZ, P, P]
+    lib.vd_stream_read.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -204,3 +206,13 @@ def vd_evict_step(k, v, n_valid, budget, variant="l2", running_sum=None, pos=Non
         ctypes.byref(desc), _ptr(n_h), _ptr(b_h), VARIANTS[variant], _ptr(running_sum),
         _ptr(pos), _ptr(scores_out), _ptr(keep_out), _ptr(workspace), ws_bytes,
         _stream(v.device, stream)))
+
+
+def vd_stream_read(buf, sink, *, stream=None):
+    """One streaming read of the whole of ``buf`` (a measurement aid: the
+    practical HBM read ceiling next to the pass); ``sink`` is a device int32
+    tensor of at least one element."""
+    if not buf.is_contiguous() or sink.dtype != torch.int32 or sink.device != buf.device:
+        raise ValueError("buf must be contiguous and sink an int32 tensor on the same device")
+    _check("vd_stream_read", load().vd_stream_read(_ptr(buf), buf.numel() * buf.element_size(),
+                                                   _ptr(sink), _stream(buf.device, stream)))

@@ -106,6 +106,16 @@ def test_status_strings_and_workspace():
     assert lib.vd_evict_step_workspace_size(ctypes.byref(good_desc())) == 0
 
 
+def test_stream_read_rejects_bad_arguments():
+    lib = vd.load()
+    good = 0x7F0000000000   # never dereferenced: validation fails first
+    assert lib.vd_stream_read(None, 16, good, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_stream_read(good + 4, 16, good, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_stream_read(good, 24, good, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_stream_read(good, 0, good, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_stream_read(good, 16, None, None) == vd.VD_ERR_INVALID_ARG
+
+
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(vd, "_lib", None)
     monkeypatch.setattr(vd, "LIB_PATH", str(tmp_path / "missing.so"))

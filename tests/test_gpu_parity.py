@@ -283,3 +283,17 @@ def test_repeat_runs_are_bitwise_identical():
     for a, b in zip(*outs):
         assert torch.equal(a.view(torch.uint8) if a.dtype == torch.bfloat16 else a,
                            b.view(torch.uint8) if b.dtype == torch.bfloat16 else b)
+
+
+def test_stream_read_reads_every_word():
+    # the sink is written iff the XOR of all words read is a fixed constant
+    magic = 0x9E3779B9
+    for words, planted in ((4, True), (4 * 1000003, True), (4 * 1000003, False)):
+        buf = torch.zeros(words, dtype=torch.int32, device=DEV)
+        if planted:
+            buf[-1] = magic - (1 << 32)      # the last word carries the constant
+        buf[0] = buf[words // 2] = 12345      # equal words in two places cancel
+        sink = torch.zeros(1, dtype=torch.int32, device=DEV)
+        vd.vd_stream_read(buf, sink)
+        torch.cuda.synchronize()
+        assert (int(sink.item()) & 0xFFFFFFFF) == (magic if planted else 0)
