@@ -176,6 +176,18 @@ def test_step_with_running_sum(orc, dt, state, variant):
     assert rep.near_ties <= 2, rep
 
 
+@pytest.mark.parametrize("dt,D,variant", [("bf16", 128, "l2"), ("f32", 256, "dir"), ("bf16", 64, "norm")])
+def test_step_at_maximum_capacity(orc, dt, D, variant):
+    """n at the ABI's slot limit (16384): every wave's selection segment is
+    full, the keys fill 64 KB of LDS and nothing is staged; one unit evicts a
+    quarter, one keeps all but one (decode argmin), one crosses the fill."""
+    C = vd.MAX_CAPACITY
+    n, N = [C, C, C], [12288, C - 1, 16000]
+    rep = run_step_case(orc, 3, 1, 1, C, D, DTYPES[dt], n, N, variant, seed=130 + D,
+                        state="incremental", count=[12288, C - 1, 9000])
+    assert rep.near_ties <= 2, rep
+
+
 def test_step_without_k_and_nhd_layout(orc):
     run_step_case(orc, 2, 3, 4, 700, 128, torch.bfloat16, [700, 650], [512, 600], "l2",
                   seed=71, layout="nhd")
