@@ -9,7 +9,7 @@
 //
 //   mean    fp64 column sums of the rows not yet summed (all n, or only the
 //           appended rows when the caller keeps a running sum), reduced in a
-//           fixed order; the first tile of old rows is already in flight
+//           fixed order; the first scoring tile is already in flight
 //                                                        (Sec. 3.2, Eq. vd)
 //   score   fp32, one DPP row reduction per row (two for Dir)  (Sec. 3.2)
 //   select  the N-th largest fp32 score on its order-preserving uint32 key:
@@ -21,10 +21,10 @@
 //           slots at or above N, ascending; only those rows move; the same
 //           loop reads the evicted rows for the running-sum update
 //
-// Row streams are software-pipelined: the loads of tile t+1 are in flight
-// while tile t is reduced, and every lane loads unconditionally (rows past
-// the end are clamped to the last row and ignored).  No MFMA: nothing here is
-// a dense contraction.
+// The row stream is software-pipelined: chunk k of tile t+1 is requested as
+// soon as chunk k of tile t is used, and every lane loads unconditionally
+// (rows past the end are clamped to the last row and ignored).  No MFMA:
+// nothing here is a dense contraction.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -40,7 +40,7 @@ template <bool V> struct BoolC { static constexpr bool value = V; };
 
 constexpr int NT = kBlock;
 constexpr int NW = kWaves;
-constexpr int kUnroll = 4;  // 16-byte loads per lane per tile (two tiles in flight)
+constexpr int kUnroll = 4;  // 16-byte rows per lane in a staged-row tile and a gather batch
 constexpr int kChunks = 2 * kUnroll;  // the pass kernel's row stream: one tile of 8 in flight
 static_assert(NT == kBins, "the selection gives every thread one histogram bin");
 
@@ -229,84 +229,6 @@ __device__ __forceinline__ uint32_t orderable(float f) {
     uint32_t b = __float_as_uint(f);
     if (b == 0x80000000u) b = 0u;
     return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
-}
-
-// ---------------------------------------------------------------- row streams
-
-// Tile t of a stream of `count` rows: slot k of this lane is element
-// t*STEP + (k*NW + wave)*RPW + lane/LPR; row_of maps an element to a row and
-// fetch(row, chunk) returns the lane's 16 bytes of it.
-template <int DT, int D, typename RowOf, typename Fetch>
-__device__ __forceinline__ void load_tile(int t, int count, RowOf row_of, Fetch fetch,
-                                          uint4 (&buf)[kUnroll]) {
-    using S = Shape<DT, D>;
-    const int base = t * S::STEP + wave_id() * S::RPW + lane_id() / S::LPR;
-    const int cl = lane_id() % S::LPR;
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-        const int e = base + k * NW * S::RPW;
-        buf[k] = fetch(row_of(e < count ? e : count - 1), cl);
-    }
-}
-
-template <int DT, int D, typename Body>
-__device__ __forceinline__ void use_tile(int t, int count, const uint4 (&buf)[kUnroll], Body body) {
-    using S = Shape<DT, D>;
-    const int base = t * S::STEP + wave_id() * S::RPW + lane_id() / S::LPR;
-#pragma unroll
-    for (int k = 0; k < kUnroll; ++k) {
-        const int e = base + k * NW * S::RPW;
-        body(e, e < count, buf[k]);
-    }
-}
-
-// Streams elements [0, count) whose tiles 0 and 1 are already loaded in `a`
-// and `b` (tile 1 only if it exists); body(e, valid, data) runs on every
-// lane, so DPP reductions inside it always see whole row groups.
-template <int DT, int D, typename RowOf, typename Fetch, typename Body>
-__device__ __forceinline__ void for_rows_pre2(int count, RowOf row_of, Fetch fetch, Body body,
-                                              uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
-    using S = Shape<DT, D>;
-    // Two tiles stay in flight.  The loop only runs while both tiles it loads
-    // exist, and the last one to three tiles are taken in straight-line code:
-    // no load is issued past the end, and every use waits for exactly its own
-    // tile (the load counter retires in order).
-    const int ntiles = (count + S::STEP - 1) / S::STEP;
-    int t = 0;
-    for (; t + 3 < ntiles; t += 2) {
-        use_tile<DT, D>(t, count, a, body);
-        load_tile<DT, D>(t + 2, count, row_of, fetch, a);
-        use_tile<DT, D>(t + 1, count, b, body);
-        load_tile<DT, D>(t + 3, count, row_of, fetch, b);
-    }
-    const int left = ntiles - t;
-    if (left == 3) {
-        use_tile<DT, D>(t, count, a, body);
-        load_tile<DT, D>(t + 2, count, row_of, fetch, a);
-        use_tile<DT, D>(t + 1, count, b, body);
-        use_tile<DT, D>(t + 2, count, a, body);
-    } else if (left == 2) {
-        use_tile<DT, D>(t, count, a, body);
-        use_tile<DT, D>(t + 1, count, b, body);
-    } else if (left == 1) {
-        use_tile<DT, D>(t, count, a, body);
-    }
-}
-
-// Loads the first two tiles of a stream (clamped like every other tile).
-template <int DT, int D, typename RowOf, typename Fetch>
-__device__ __forceinline__ void load_first2(int count, RowOf row_of, Fetch fetch,
-                                            uint4 (&a)[kUnroll], uint4 (&b)[kUnroll]) {
-    load_tile<DT, D>(0, count, row_of, fetch, a);
-    load_tile<DT, D>(1, count, row_of, fetch, b);
-}
-
-template <int DT, int D, typename RowOf, typename Fetch, typename Body>
-__device__ __forceinline__ void for_rows(int count, RowOf row_of, Fetch fetch, Body body) {
-    if (count <= 0) return;
-    uint4 a[kUnroll], b[kUnroll];
-    load_first2<DT, D>(count, row_of, fetch, a, b);
-    for_rows_pre2<DT, D>(count, row_of, fetch, body, a, b);
 }
 
 // x + (x of lane ^ 8, 16 or 32): each lane pair ends with the same bits.
@@ -614,9 +536,9 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // the mean (staged in LDS when they fit), then the rows still to be
     // scored: [0, count) when the first part was staged, all of [0, n)
     // otherwise.  The state's token count and column sums are read first.  The
-    // first two tiles go out right behind them for the steady-state guess
-    // count = min(N, n) and go out again only if the guess was wrong, so that
-    // either way exactly two tiles are in flight, in the same order, and every
+    // first tile goes out right behind them for the steady-state guess
+    // count = min(N, n) and goes out again only if the guess was wrong, so that
+    // either way exactly one tile is in flight, in the same order, and every
     // wait counts exactly.  Nothing branches before these loads (a unit with
     // no rows reads row 0 of its slab and ignores it): the kernel arguments
     // arrive in one batch and the row tiles go out right behind them.
