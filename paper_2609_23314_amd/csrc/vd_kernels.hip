@@ -547,14 +547,19 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     const double st_col = stp[st ? min((int)threadIdx.x, D) : 0];
     const int lastrow = max(n - 1, 0);
     constexpr int kStep = S::GROUPS * kChunks;  // rows per tile of the stream
+    // A first part of at most one row per lane group (a decode step appends
+    // one row) is read by a single chunk issued ahead of the first tile, so
+    // that the stream starts with rows to score instead of a tile of repeats.
     struct Plan {
         int cnt, fresh, tiles_f, second, tiles;  // second: rows of the scoring part
+        bool small;                              // first part in one chunk, staged
     };
     auto plan_for = [&](int cnt) __attribute__((always_inline)) {
         Plan q;
         q.cnt = cnt;
         q.fresh = n - cnt;
-        q.tiles_f = (q.fresh + kStep - 1) / kStep;
+        q.small = q.fresh > 0 && q.fresh <= S::GROUPS && q.fresh <= arg_stash;
+        q.tiles_f = q.small ? 0 : (q.fresh + kStep - 1) / kStep;
         q.second = !need_scores ? 0 : (q.fresh <= arg_stash ? cnt : n);
         q.tiles = q.tiles_f + (q.second + kStep - 1) / kStep;
         return q;
@@ -573,8 +578,13 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
 #pragma unroll
         for (int k = 0; k < kChunks; ++k) buf[k] = load_chunk(q, t, k);
     };
+    const int eb = wave_id() * S::RPW + lane / S::LPR;  // this lane's row group
+    auto load_small = [&](const Plan &q) __attribute__((always_inline)) -> uint4 {
+        return load_stream(vb, row_off(min(q.cnt + eb, lastrow), ss32, cl));
+    };
     const Plan guessed = plan_for(st ? min(N, n) : 0);
-    uint4 buf[kChunks];
+    uint4 buf[kChunks], fc;
+    if (guessed.small) fc = load_small(guessed);
     load_v(guessed, 0, buf);
 
     if (n <= 0) {
@@ -596,6 +606,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     if (st) count = (craw >= 0.0 && craw <= (double)n && craw == (double)(int)craw) ? (int)craw : 0;
     const Plan q = count == guessed.cnt ? guessed : plan_for(count);
     if (count != guessed.cnt) {
+        if (q.small) fc = load_small(q);
         load_v(q, 0, buf);
     }
     const int fresh = q.fresh;
@@ -760,7 +771,6 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         finish_mean();
         for (int i = 0; i < stash_tiles; ++i) score_stash_tile(i);
     };
-    const int eb = wave_id() * S::RPW + lane / S::LPR;
     // chunk k of scoring tile tn < tiles (no clamping to other parts needed)
     auto load_scored = [&](int tn, int k, uint32_t z) __attribute__((always_inline)) -> uint4 {
         const int e = (tn - q.tiles_f) * kStep + k * NW * S::RPW + eb;
@@ -814,6 +824,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     {
         const int T = q.tiles;
         int t = 0;
+        if (q.small) mean_body(eb, eb < fresh, fc);
         for (; t < q.tiles_f && t + 1 < T; ++t) use_fresh(t, std::true_type{});
         if (t < q.tiles_f) use_fresh(t++, std::false_type{});  // no scoring part follows
         switch_parts();
