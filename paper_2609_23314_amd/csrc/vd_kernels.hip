@@ -332,10 +332,12 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         uint32_t *hn = (pass & 1) ? H.hist : hist2;
         const int bits = 32 - __clz(hi - lo);  // bits of the largest offset
         const int shift = bits > 10 ? bits - 10 : 0;
+        // a lane outside the range adds 0 to a bin of its own (no lane mask switched)
         for (int jb = j0; jb < j1; jb += 64) {
             const int j = jb + lane;
-            const uint32_t k = j < j1 ? keys[j] : 0u;
-            if (j < j1 && k >= lo && k <= hi) atomicAdd(&hc[(k - lo) >> shift], 1u);
+            const uint32_t k = keys[j < j1 ? j : j0];
+            const bool in = j < j1 && k >= lo && k <= hi;
+            atomicAdd(&hc[in ? (k - lo) >> shift : (uint32_t)lane], in ? 1u : 0u);
         }
         __syncthreads();
         // wave w owns bins kBins-1-64w .. kBins-64-64w (descending keys); the
@@ -370,7 +372,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         for (int jb = j0; jb < j1; jb += 64) {
             const int j = jb + lane;
             const bool v = j < j1;
-            const uint32_t k = v ? keys[j] : 0u;
+            const uint32_t k = keys[v ? j : j0];
             const bool c = v && k >= lo && k <= hi;
             sev += __popcll(__ballot(v && k < lo));
             smv += __popcll(__ballot(v && k > hi && j >= N));
@@ -469,18 +471,20 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         mv_tot = sum_below16(m_i, NW);
     }
     // each wave writes its part of the lists
+    // (a lane with nothing to list stores to its own word of the histogram,
+    // which nothing reads any more, so that no lane mask is switched)
     for (int jb = j0; jb < j1; jb += 64) {
         const int j = jb + lane;
         const bool v = j < j1;
-        const uint32_t k = v ? keys[j] : 0u;
+        const uint32_t k = keys[v ? j : j0];
         const bool keep = v && (k > T || (k == T && (uint32_t)j <= J));
         const bool ev = v && !keep;
         const bool mv = keep && j >= N;
         const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
         const uint32_t rev = ev_off + ballot_rank(mev);
         const uint32_t rmv = mv_off + ballot_rank(mmv);
-        if (ev && rev < (uint32_t)evict_cap) evl[rev] = (uint32_t)j;
-        if (mv && rmv < (uint32_t)move_cap) mvl[rmv] = (uint32_t)j;
+        *((ev && rev < (uint32_t)evict_cap) ? evl + rev : H.hist + lane) = (uint32_t)j;
+        *((mv && rmv < (uint32_t)move_cap) ? mvl + rmv : H.hist + 64 + lane) = (uint32_t)j;
         if (keep_out && v) keep_out[j] = keep ? 1 : 0;
         ev_off += (uint32_t)__popcll(mev);
         mv_off += (uint32_t)__popcll(mmv);
