@@ -151,6 +151,33 @@ def test_compact_matches_oracle_exactly(orc, dt, D):
         assert np.array_equal(post_pos[u], rp), f"pos of unit {u}"
 
 
+def test_compact_with_unbalanced_masks(orc):
+    """Masks that keep more or fewer than N slots: only min(#holes, #movers)
+    rows move, the rest of the slab stays as it was."""
+    S, L, H, C, D = 1, 2, 2, 1200, 128
+    n, N = [1200], [800]
+    k, v = make_cache(S, L, H, C, D, torch.bfloat16, n, seed=34)
+    U = S * L * H
+    rng = np.random.default_rng(35)
+    frac = [0.2, 0.5, 0.9, 1.0]   # of slots kept: few movers ... no holes
+    keep = torch.zeros((U, C), dtype=torch.uint8)
+    for u in range(U):
+        keep[u, :n[0]] = torch.from_numpy((rng.random(n[0]) < frac[u]).astype(np.uint8))
+    keep = keep.to(DEV)
+    pos = torch.arange(C, dtype=torch.int32, device=DEV).repeat(U, 1).contiguous()
+    pre_k, pre_v, pre_pos = units(to_np(k)), units(to_np(v)), to_np(pos)
+    vd.vd_compact(k, v, keep, n, N, pos)
+    torch.cuda.synchronize()
+    post_k, post_v, post_pos = units(to_np(k)), units(to_np(v)), to_np(pos)
+    kn = to_np(keep)
+    for u in range(U):
+        rk, rv, rp = pre_k[u].copy(), pre_v[u].copy(), pre_pos[u].copy()
+        orc.compact(rk, rv, n[0], N[0], kn[u, :n[0]], rp)
+        assert np.array_equal(post_k[u].view(np.uint8), rk.view(np.uint8)), f"K of unit {u}"
+        assert np.array_equal(post_v[u].view(np.uint8), rv.view(np.uint8)), f"V of unit {u}"
+        assert np.array_equal(post_pos[u], rp), f"pos of unit {u}"
+
+
 # ------------------------------------------------------------------ vd_evict_step
 
 @pytest.mark.parametrize("dt", list(DTYPES))
