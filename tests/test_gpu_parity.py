@@ -122,6 +122,32 @@ def test_select_matches_oracle_exactly(orc, ties):
         assert np.all(kg[u, nu[u]:] == 7)
 
 
+def test_select_negative_scores_and_signed_zeros(orc):
+    """Scores of any sign (a caller's own ranking), with +0 and -0 mixed: the
+    two zeros are one value, so they tie and the lower slot wins."""
+    S, L, H, C, D = 1, 1, 4, 1500, 64
+    n, N = [1500], [700]
+    v = torch.zeros((S, L, H, C, D), dtype=torch.float32, device=DEV)
+    rng = np.random.default_rng(37)
+    rows = []
+    for u in range(4):
+        x = rng.standard_normal(C).astype(np.float32) * (10.0 ** (u - 1))
+        x[rng.random(C) < 0.3] = 0.0
+        x[rng.random(C) < 0.3] = -0.0
+        if u == 3:
+            x[:] = np.where(rng.random(C) < 0.5, np.float32(0.0), np.float32(-0.0))  # all zero
+        rows.append(x)
+    sc = torch.from_numpy(np.stack(rows)).to(DEV)
+    keep = torch.full((4, C), 7, dtype=torch.uint8, device=DEV)
+    vd.vd_select_topn(v, sc, n, N, keep)
+    torch.cuda.synchronize()
+    kg = to_np(keep)
+    for u in range(4):
+        want = orc.select_topn(rows[u][:n[0]].astype(np.float64), N[0])
+        assert np.array_equal(kg[u, :n[0]], want), f"unit {u}"
+    assert np.array_equal(kg[3, :n[0]], (np.arange(n[0]) < N[0]).astype(np.uint8))
+
+
 # ------------------------------------------------------------------ vd_compact
 
 @pytest.mark.parametrize("dt", list(DTYPES))
