@@ -176,6 +176,38 @@ def test_llama_prefill_oracle_forced_boundaries(orc):
         assert rep.units == 3 * U and rep.near_ties <= U // 10, rep
 
 
+def test_llama_prefill_whole_prompt_state_stays_exact():
+    """The whole 32768-token prompt run free on the GPU (64 blocks, 60
+    evicting passes, the running sum carried from pass to pass): after every
+    pass the state equals the fp64 sum of the rows left in [0, N) and counts
+    N, and every pass keeps exactly N rows.  A property of any correct pass,
+    so it needs no oracle trajectory and holds at the full size."""
+    w = synth.llama_prefill()
+    N, B, D = w.budget[0], w.block, w.head_dim
+    U, C = w.units, w.capacity
+    k, v = synth.empty_cache(w, DEV)
+    rs = torch.zeros((U, D + 1), dtype=torch.float64, device=DEV)
+    keep = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
+    n_o, passes = 0, 0
+    for blk in range(w.prompt[0] // B):
+        t0 = blk * B
+        k[0, :, :, n_o:n_o + B] = synth.block_rows(w, "k", 0, blk, t0, t0 + B, DEV)
+        v[0, :, :, n_o:n_o + B] = synth.block_rows(w, "v", 0, blk, t0, t0 + B, DEV)
+        n = n_o + B
+        vd.vd_evict_step(k, v, [n], [N], "l2", running_sum=rs, keep_out=keep)
+        n_o = min(n, N)
+        if n > N:
+            passes += 1
+            assert int(keep[:, :n].sum().item()) == U * N, f"block {blk}"
+        want = v[0, :, :, :n_o].double().sum(dim=2).reshape(U, D)
+        got = rs[:, :D]
+        scale = v[0, :, :, :n_o].double().abs().sum(dim=2).reshape(U, D).clamp_min(1.0)
+        err = ((got - want).abs() / scale).max().item()
+        assert err < 1e-12, f"block {blk}: state off by {err:.3g} (relative to the sum of |v|)"
+        assert torch.all(rs[:, D] == n_o), f"block {blk}: count"
+    assert passes == 60
+
+
 # ------------------------------------------------------------------ decode
 
 def test_decode_step_sampled_units(orc):
