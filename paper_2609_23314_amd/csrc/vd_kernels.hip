@@ -601,11 +601,6 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
         return;
     }
-    // one early read of the unit's K slab warms its address translation before
-    // the gather moves K rows; the value is only looked at after scoring
-    uint32_t kprobe = 0u;
-    if (evict && p.k && threadIdx.x == 0)
-        kprobe = __builtin_nontemporal_load(reinterpret_cast<const uint32_t *>(p.k + off + (int64_t)N * ss32));
     int count = 0;
     if (st) count = (craw >= 0.0 && craw <= (double)n && craw == (double)(int)craw) ? (int)craw : 0;
     const Plan q = count == guessed.cnt ? guessed : plan_for(count);
@@ -835,10 +830,6 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         for (; t + 1 < T; ++t) use_scored(t, std::true_type{});
         if (t < T) use_scored(t, std::false_type{});  // the last tile: no load past the end
     }
-    // the probe value is consumed only here (the empty asm keeps the compiler
-    // from testing it, and so waiting for it, next to the load)
-    asm volatile("" : "+v"(kprobe));
-    if (kprobe == 0x7FC00001u) H.bc[127] = kprobe;  // keeps the probe load; nothing reads bc[127]
     if (to_lds) {  // what the selection reads after the barrier below
         kmin = wave_min_u32(kmin);
         kmax = wave_max_u32(kmax);
