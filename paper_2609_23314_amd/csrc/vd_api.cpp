@@ -103,7 +103,8 @@ vd_status plan_step_lds(const vd_cache_desc *d, UnitParams &p, int ns, bool scor
     const int64_t lists_bytes = align16(int64_t(evict_cap + move_cap) * 4);
     const int64_t used = int64_t(sizeof(vd::LdsHead)) + keys_bytes + lists_bytes;
     if (used > vd::kLdsBytes) return VD_ERR_UNSUPPORTED;
-    const int64_t stash_rows = (int64_t(want_rows) * row_bytes <= vd::kLdsBytes - used) ? want_rows : 0;
+    // as many of the rows to stage as fit (the kernel streams the rest twice)
+    const int64_t stash_rows = std::min<int64_t>(want_rows, (vd::kLdsBytes - used) / row_bytes);
     p.off_keys = int32_t(sizeof(vd::LdsHead));
     p.off_lists = int32_t(p.off_keys + keys_bytes);
     p.off_stash = int32_t(p.off_lists + lists_bytes);

@@ -554,20 +554,25 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // A first part of at most one row per lane group (a decode step appends
     // one row) is read by a single chunk issued ahead of the first tile, so
     // that the stream starts with rows to score instead of a tile of repeats.
+    // The first part is staged in LDS as far as it fits (its first `staged`
+    // rows); the scoring part then covers the old rows and the rest of the
+    // first part: element e of it is row e below cnt and row e + staged above.
     struct Plan {
-        int cnt, fresh, tiles_f, second, tiles;  // second: rows of the scoring part
-        bool small;                              // first part in one chunk, staged
+        int cnt, fresh, staged, tiles_f, second, tiles;  // second: rows of the scoring part
+        bool small;                                      // first part in one chunk, staged
     };
     auto plan_for = [&](int cnt) __attribute__((always_inline)) {
         Plan q;
         q.cnt = cnt;
         q.fresh = n - cnt;
+        q.staged = min(q.fresh, arg_stash);
         q.small = q.fresh > 0 && q.fresh <= S::GROUPS && q.fresh <= arg_stash;
         q.tiles_f = q.small ? 0 : (q.fresh + kStep - 1) / kStep;
-        q.second = !need_scores ? 0 : (q.fresh <= arg_stash ? cnt : n);
+        q.second = !need_scores ? 0 : n - q.staged;
         q.tiles = q.tiles_f + (q.second + kStep - 1) / kStep;
         return q;
     };
+    auto srow = [&](const Plan &q, int e) __attribute__((always_inline)) { return e < q.cnt ? e : e + q.staged; };
     // chunk k of tile t of the stream; a tile past the end reads the last row
     // (never used)
     auto load_chunk = [&](const Plan &q, int t, int k, uint32_t z = 0u) __attribute__((always_inline)) -> uint4 {
@@ -575,7 +580,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         const int lim = first ? q.fresh : q.second;
         const int rbase = first ? q.cnt : 0;
         const int e = (first ? t : t - q.tiles_f) * kStep + (k * NW + wave_id()) * S::RPW + lane / S::LPR;
-        const int r = (t < q.tiles && lim > 0) ? rbase + min(e, lim - 1) : lastrow;
+        const int ec = min(e, lim - 1);
+        const int r = (t < q.tiles && lim > 0) ? (first ? rbase + ec : srow(q, ec)) : lastrow;
         return load_stream(vb, row_off(r, ss32, cl) + z);
     };
     auto load_v = [&](const Plan &q, int t, uint4 (&buf)[kChunks]) __attribute__((always_inline)) {
@@ -609,11 +615,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         load_v(q, 0, buf);
     }
     const int fresh = q.fresh;
-    const bool stashed = fresh <= arg_stash;
+    const int staged = q.staged;             // first-part rows in LDS
+    const bool stashed = staged == fresh;    // all of them
     auto sfetch = [&](int r, int c) __attribute__((always_inline)) -> uint4 {
         return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
     };
-    auto fresh_row = [&](int e) __attribute__((always_inline)) { return min(count + e, lastrow); };
+    auto fresh_row = [&](int e) __attribute__((always_inline)) { return count + min(e, max(staged - 1, 0)); };
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
     // keys go to LDS for the selection and for the score output: no global
     // store sits between the row loads of the stream (a store in flight makes
@@ -633,7 +640,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (valid) {
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
-            if (stashed) *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
+            if (e < staged) *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
         }
     };
     auto finish_mean = [&]() __attribute__((always_inline)) {
@@ -726,13 +733,14 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         }
         return a;
     };
-    auto score4 = [&](const float (&a)[4], int e0, int lim, int rbase) __attribute__((always_inline)) {
+    // (the row of element e is rbase + e, plus gap at and above gap_at)
+    auto score4 = [&](const float (&a)[4], int e0, int lim, int rbase, int gap_at, int gap) __attribute__((always_inline)) {
         const float s = score_sqrt(row_sums4<S::LPR>(a, cl));
         const int e = e0 + quad_row(cl) * NW * S::RPW;
         if (cl < 4 && e < lim) {
             const uint32_t key = score_key(s);
             if (to_lds) {
-                keys[rbase + e] = key;
+                keys[rbase + e + (e >= gap_at ? gap : 0)] = key;
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
             }
@@ -748,17 +756,17 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             float a[4];
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) a[k] = partial(w4[k]);
-            score4(a, e0, fresh, count);
+            score4(a, e0, staged, count, staged, 0);
         } else {
 #pragma unroll
             for (int k = 0; k < kUnroll; ++k) {
                 const int e = e0 + k * NW * S::RPW;
-                on_fresh(e, e < fresh, sfetch(fresh_row(e), cl));
+                on_fresh(e, e < staged, sfetch(fresh_row(e), cl));
             }
         }
     };
-    const bool score_stash = stashed && need_scores;
-    const int stash_tiles = score_stash ? (fresh + S::STEP - 1) / S::STEP : 0;
+    const bool score_stash = staged > 0 && need_scores;
+    const int stash_tiles = score_stash ? (staged + S::STEP - 1) / S::STEP : 0;
     // Tile t is used chunk by chunk, and chunk k of tile t + 1 is requested
     // into the same registers as soon as chunk k of t is used: the row loads
     // in flight never drop below one tile less one chunk, and the loads cross
@@ -773,7 +781,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // chunk k of scoring tile tn < tiles (no clamping to other parts needed)
     auto load_scored = [&](int tn, int k, uint32_t z) __attribute__((always_inline)) -> uint4 {
         const int e = (tn - q.tiles_f) * kStep + k * NW * S::RPW + eb;
-        return load_stream(vb, row_off(min(e, q.second - 1), ss32, cl) + z);
+        return load_stream(vb, row_off(srow(q, min(e, q.second - 1)), ss32, cl) + z);
     };
     // The load that refills a chunk's registers takes its address through a
     // zero that the compiler sees as computed from the chunk's results, so it
@@ -806,13 +814,13 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                         __builtin_amdgcn_sched_barrier(0);
                     }
                 }
-                score4(a, e0 + h * NW * S::RPW, q.second, 0);
+                score4(a, e0 + h * NW * S::RPW, q.second, 0, q.cnt, q.staged);
             }
         } else {
 #pragma unroll
             for (int k = 0; k < kChunks; ++k) {
                 const int e = e0 + k * NW * S::RPW;
-                const float sc = on_row(e, e < q.second, buf[k]);
+                const float sc = on_row(srow(q, e), e < q.second, buf[k]);
                 if constexpr (more()) {
                     buf[k] = load_scored(t + 1, k, zero_after(sc));
                     __builtin_amdgcn_sched_barrier(0);
@@ -900,7 +908,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         int32_t *pos = p.pos ? p.pos + u * cap : nullptr;
         const int g = wave_id() * S::RPW + lane / S::LPR;  // row group of this lane
         auto vfetch = [&](int r) __attribute__((always_inline)) -> uint4 {
-            return (stashed && r >= count) ? sfetch(r, cl) : load_stream(vb, row_off(r, ss32, cl));
+            return (r >= count && r < count + staged) ? sfetch(r, cl) : load_stream(vb, row_off(r, ss32, cl));
         };
         double acc[S::EPL];
 #pragma unroll

@@ -241,6 +241,19 @@ def test_step_at_maximum_capacity(orc, dt, D, variant):
     assert rep.near_ties <= 2, rep
 
 
+@pytest.mark.parametrize("dt", list(DTYPES))
+@pytest.mark.parametrize("state", ["none", "incremental"])
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_step_partial_staging(orc, dt, state, variant):
+    """Rows to stage (the appended part, or all n rows without a state) that do
+    not all fit in LDS at head_dim 256: the first ones are staged and the rest
+    is streamed twice (for the mean, then for the scores)."""
+    n, N, count = [600, 450], [400, 300], [300, 100]
+    rep = run_step_case(orc, 2, 1, 2, 600, 256, DTYPES[dt], n, N, variant, seed=140,
+                        state=state, count=count if state != "none" else None)
+    assert rep.near_ties <= 2, rep
+
+
 def test_step_without_k_and_nhd_layout(orc):
     run_step_case(orc, 2, 3, 4, 700, 128, torch.bfloat16, [700, 650], [512, 600], "l2",
                   seed=71, layout="nhd")
