@@ -942,9 +942,11 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
 #pragma unroll
                 for (int k = 0; k < KV; ++k)
                     km[k] = load_stream(ksrc, row_off(src[k], ss32, cl));
-                if constexpr (!STASH) {
+                if constexpr (!STASH) {  // staged movers (a partly staged block) come from LDS
 #pragma unroll
-                    for (int k = 0; k < KV; ++k) vm[k] = load_stream(vb, row_off(src[k], ss32, cl));
+                    for (int k = 0; k < KV; ++k)
+                        vm[k] = src[k] < count + staged ? sfetch(src[k], cl)
+                                                        : load_stream(vb, row_off(src[k], ss32, cl));
                 }
                 if (pos) {
 #pragma unroll
