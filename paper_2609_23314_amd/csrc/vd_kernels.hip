@@ -537,9 +537,9 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
 
     // The rows are read in one software-pipelined stream of tiles over two
     // parts: first the rows not yet in the running sum, [count, n), which give
-    // the mean (staged in LDS when they fit), then the rows still to be
-    // scored: [0, count) when the first part was staged, all of [0, n)
-    // otherwise.  The state's token count and column sums are read first.  The
+    // the mean (staged in LDS as far as they fit), then the rows still to be
+    // scored: [0, count) and the first part's unstaged rows.  The state's
+    // token count and column sums are read first.  The
     // first tile goes out right behind them for the steady-state guess
     // count = min(N, n) and goes out again only if the guess was wrong, so that
     // either way exactly one tile is in flight, in the same order, and every
