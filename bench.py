@@ -19,6 +19,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -41,10 +42,15 @@ def log(*a):
 
 
 def kernel_hash() -> str:
+    """Hash of the kernel and host sources with comments and blank space
+    removed, so that profiles stay tied to the code, not to its comments."""
     h = hashlib.sha256()
     for f in (KERNEL_SRC, os.path.join(ROOT, "paper_2609_23314_amd", "csrc", "vd_api.cpp")):
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
