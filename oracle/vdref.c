@@ -22,10 +22,17 @@
  *      evicted slots below N, ascending, receive the kept slots at or above N,
  *      ascending (the layout reading of "gather" used by this project).
  *
+ * Geometry diagnostics of one unit (Sec. 3.1 and the bos-cosim equation of
+ * Sec. 4), from their definitions: sigma_X = std_i ||x_i - x_bar|| for X = K
+ * and V (the population standard deviation over the n tokens), the mean of
+ * those distances, and bos-cosim = cos(k_0, (1/(n-1)) sum_{i>0} k_i).
+ *
  * Readings of points the paper leaves open:
  *   - Dir when ||v_j|| * ||v_bar|| == 0: cos is taken as 0, so s_j = 1.
  *   - Norm keeps the largest norms.
  *   - n <= N is a no-op (eviction happens only when the cache exceeds N).
+ *   - std is the population one (divide by n); bos-cosim is 0 when either
+ *     vector is zero or n < 2.
  *
  * Pins: every function here is checked by the CPU tests against identities
  * and brute force that do not reuse this code (minimal-disturbance identity
@@ -303,4 +310,73 @@ int vdref_evict_step(void *k, void *v, int dtype, int64_t U, int64_t cap, int d,
         free(keepu);
     }
     return status;
+}
+
+/* ---- geometry diagnostics (Sec. 3.1, Sec. 4 bos-cosim) ----------------- */
+
+/* Mean and population standard deviation over i of ||x_i - x_bar||. */
+static void dispersion(const void *x, int dtype, int64_t n, int d, int64_t row_stride,
+                       double *mean_dist, double *sigma)
+{
+    double *xbar = (double *)malloc(sizeof(double) * (size_t)d);
+    double *dist = (double *)malloc(sizeof(double) * (size_t)n);
+    if (!xbar || !dist) {
+        free(xbar);
+        free(dist);
+        *mean_dist = *sigma = 0.0;
+        return;
+    }
+    vdref_mean(x, dtype, n, d, row_stride, xbar);
+    double sum = 0.0;
+    for (int64_t i = 0; i < n; ++i) {
+        double acc = 0.0;
+        for (int c = 0; c < d; ++c) {
+            double diff = get_elem(x, dtype, i * row_stride + c) - xbar[c];
+            acc += diff * diff;
+        }
+        dist[i] = sqrt(acc);
+        sum += dist[i];
+    }
+    double mu = sum / (double)n;
+    double var = 0.0;
+    for (int64_t i = 0; i < n; ++i)
+        var += (dist[i] - mu) * (dist[i] - mu);
+    *mean_dist = mu;
+    *sigma = sqrt(var / (double)n);
+    free(xbar);
+    free(dist);
+}
+
+/*
+ * out[0] = sigma_K, out[1] = sigma_V, out[2] = mean ||k_i - k_bar||,
+ * out[3] = mean ||v_i - v_bar||, out[4] = bos-cosim; all zero when n == 0.
+ */
+int vdref_geometry(const void *k, const void *v, int dtype, int64_t n, int d,
+                   int64_t row_stride, double *out)
+{
+    if (n < 0 || d <= 0 || !k || !v || !out)
+        return VDREF_BAD_ARG;
+    for (int i = 0; i < 5; ++i)
+        out[i] = 0.0;
+    if (n == 0)
+        return VDREF_OK;
+    dispersion(k, dtype, n, d, row_stride, &out[2], &out[0]);
+    dispersion(v, dtype, n, d, row_stride, &out[3], &out[1]);
+    if (n >= 2) {
+        /* cos(k_0, (1/(n-1)) sum_{i>0} k_i) */
+        double dot = 0.0, n0 = 0.0, nm = 0.0;
+        for (int c = 0; c < d; ++c) {
+            double m = 0.0;
+            for (int64_t i = 1; i < n; ++i)
+                m += get_elem(k, dtype, i * row_stride + c);
+            m /= (double)(n - 1);
+            double k0 = get_elem(k, dtype, c);
+            dot += k0 * m;
+            n0 += k0 * k0;
+            nm += m * m;
+        }
+        double denom = sqrt(n0) * sqrt(nm);
+        out[4] = denom > 0.0 ? dot / denom : 0.0;
+    }
+    return VDREF_OK;
 }

@@ -59,8 +59,9 @@ class Oracle:
         lib.vdref_compact.argtypes = [_p, _p, _i32, _i64, _i64, _i32, _i64, _p, _p]
         lib.vdref_evict_step.argtypes = [_p, _p, _i32, _i64, _i64, _i32, _p, _p, _i32,
                                          _p, _p, _p, _p, _i32]
+        lib.vdref_geometry.argtypes = [_p, _p, _i32, _i64, _i32, _i64, _p]
         for f in ("vdref_mean", "vdref_score", "vdref_select_topn", "vdref_compact",
-                  "vdref_evict_step"):
+                  "vdref_evict_step", "vdref_geometry"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = path
@@ -111,6 +112,18 @@ class Oracle:
         if self.lib.vdref_compact(_ptr(k), _ptr(v), _dtype_tag(ref), n, N, d, d,
                                   _ptr(keep), _ptr(pos)):
             raise ValueError("vdref_compact rejected its arguments")
+
+    def geometry(self, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+        """[sigma_K, sigma_V, mean ||k - k_bar||, mean ||v - v_bar||, bos-cosim]
+        of the n rows of ``k`` and ``v`` ([n, d] each)."""
+        k, v = np.ascontiguousarray(k), np.ascontiguousarray(v)
+        if k.shape != v.shape or k.dtype != v.dtype:
+            raise ValueError("k and v must share shape and dtype")
+        n, d = v.shape
+        out = np.empty(5, np.float64)
+        if self.lib.vdref_geometry(_ptr(k), _ptr(v), _dtype_tag(v), n, d, d, _ptr(out)):
+            raise ValueError("vdref_geometry rejected its arguments")
+        return out
 
     def evict_step(self, k, v, n_unit, N_unit, variant="l2", pos=None, nthreads=0):
         """One eviction pass over U units, in place.
@@ -176,3 +189,7 @@ def compact(k, v, n, N, keep, pos=None):
 
 def evict_step(k, v, n_unit, N_unit, variant="l2", pos=None, nthreads=0):
     return load().evict_step(k, v, n_unit, N_unit, variant, pos, nthreads)
+
+
+def geometry(k, v):
+    return load().geometry(k, v)

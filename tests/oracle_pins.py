@@ -14,6 +14,8 @@ Pins and what they fix:
   selection           stable sort, brute force over subsets, n = N + 1, n <= N
   compaction          row multiset / pairing / slot-reuse layout properties
   decoding            bf16 and fp32 element values against torch's conversion
+  geometry            sigma_K / sigma_V / bos-cosim (Sec. 3.1, Sec. 4): hand values,
+                      closed forms, invariances and special cases
 """
 import itertools
 import json
@@ -329,11 +331,60 @@ def check_evict_step_batch(orc):
             assert np.array_equal(v[u, n:], v_pre[u, n:])  # beyond n: untouched
 
 
+def check_geometry(orc):
+    """sigma_X = std_i ||x_i - x_bar|| (population std) and bos-cosim =
+    cos(k_0, mean of k_1..k_{n-1}) against values derived by hand and
+    properties that fix them."""
+    r2 = np.sqrt(2.0)
+    # W1 rows as V, W2 rows as K: distances V [r2, 1, 1, 2 r2], K [1, 1, 0, r2];
+    # content mean of K = (1, 4/3), so bos-cosim = 1 / (5/3)
+    V = _f32([[0, 0], [1, 0], [0, 1], [3, 3]])
+    K = _f32([[1, 0], [0, 1], [1, 1], [2, 2]])
+    mu_v, mu_k = (2 + 3 * r2) / 4, (2 + r2) / 4
+    want = [np.sqrt(1.0 - mu_k ** 2), np.sqrt(3.0 - mu_v ** 2), mu_k, mu_v, 0.6]
+    assert _rel_close(orc.geometry(K, V), want, 1e-12), orc.geometry(K, V)
+    # one channel, rows -2, -1, 1, 2: distances 2, 1, 1, 2 -> mean 1.5, population std 0.5
+    x = _f32([[-2], [-1], [1], [2]])
+    g = orc.geometry(x, x)
+    assert _rel_close(g[:4], [0.5, 0.5, 1.5, 1.5], 1e-12), g
+    # two rows: both at half their distance from the mean, so sigma = 0
+    g = orc.geometry(_f32([[0, 0], [3, 4]]), _f32([[1, 1], [1, 1]]))
+    assert _rel_close(g[:4], [0.0, 0.0, 2.5, 0.0], 1e-12, 1e-12), g
+    # one token: nothing spreads and there is no content mean
+    assert np.all(orc.geometry(_f32([[1, 2]]), _f32([[3, 4]])) == 0.0)
+    # bos-cosim: k_0 against the content mean, along it, opposite, zero
+    c = _f32([[1, 2], [3, 1], [2, 3]])   # content mean (2, 2)
+    for k0, cos in (([4, 4], 1.0), ([-1, -1], -1.0), ([0, 0], 0.0), ([2, -2], 0.0)):
+        g = orc.geometry(_f32(np.vstack([k0, c])), _f32(np.vstack([k0, c])))
+        assert abs(g[4] - cos) < 1e-12, (k0, g[4])
+    # invariances: translation and permutation keep sigma and the mean distance,
+    # scaling by a multiplies them by |a| and keeps bos-cosim
+    rng = np.random.default_rng(31)
+    k = _f32(rng.standard_normal((40, 6)))
+    v = _f32(rng.standard_normal((40, 6)) * 3.0)
+    g = orc.geometry(k, v)
+    t = _f32(k + rng.standard_normal(6).astype(np.float32) * 0.5)
+    u = _f32(v + rng.standard_normal(6).astype(np.float32) * 0.5)
+    assert _rel_close(orc.geometry(t, u)[:4], g[:4], 1e-5)
+    perm = np.concatenate([[0], 1 + rng.permutation(39)])
+    assert _rel_close(orc.geometry(k[perm], v[perm]), g, 1e-12, 1e-15)
+    for a in (2.0, -0.5):
+        ga = orc.geometry(_f32(k * a), _f32(v * a))
+        assert _rel_close(ga[:4], np.abs(a) * g[:4], 1e-6)
+        assert abs(ga[4] - g[4]) < 1e-6
+    # bf16 rows give the same statistics as their fp32 values
+    kb = (k.view(np.uint32) >> 16).astype(np.uint16)
+    vb = (v.view(np.uint32) >> 16).astype(np.uint16)
+    kf = _f32((kb.astype(np.uint32) << 16).view(np.float32))
+    vf = _f32((vb.astype(np.uint32) << 16).view(np.float32))
+    assert _rel_close(orc.geometry(kb, vb), orc.geometry(kf, vf), 1e-12, 1e-15)
+
+
 ALL_CHECKS = [
     check_decode, check_mean_library, check_worked_examples,
     check_minimal_disturbance, check_law_of_cosines, check_dirichlet,
     check_invariances, check_select_vs_sort, check_select_bruteforce,
-    check_select_special, check_compact, check_evict_step_batch,
+    check_select_special, check_compact, check_evict_step_batch, check_geometry,
 ]
 
 

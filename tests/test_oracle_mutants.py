@@ -45,6 +45,12 @@ MUTANTS = [
     ("bf16_wrong_shift", "uint32_t w = ((uint32_t)bits) << 16;", "uint32_t w = ((uint32_t)bits) << 15;"),
     ("unit_offset_wrong", "char *vu = (char *)v + (size_t)(u * cap * d) * es;",
      "char *vu = (char *)v + (size_t)(u * d) * es;"),
+    ("sigma_sample_std", "*sigma = sqrt(var / (double)n);", "*sigma = sqrt(var / (double)(n - 1));"),
+    ("dispersion_squared", "dist[i] = sqrt(acc);", "dist[i] = acc;"),
+    ("bos_mean_includes_bos", "for (int64_t i = 1; i < n; ++i)\n                m +=",
+     "for (int64_t i = 0; i < n; ++i)\n                m +="),
+    ("sigma_k_of_v", "dispersion(k, dtype, n, d, row_stride, &out[2], &out[0]);",
+     "dispersion(v, dtype, n, d, row_stride, &out[2], &out[0]);"),
 ]
 
 
