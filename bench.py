@@ -291,6 +291,90 @@ def load_traffic(workload: str):
     return t.get("bytes_per_launch")
 
 
+def geometry_bench(w, args, dev):
+    """Times vd_geometry (sigma_K, sigma_V, mean distances and bos-cosim of
+    every unit; Sec. 3.1, Sec. 4) over the workload's cache with every unit
+    filled to capacity by the workload's generator.  The passes run back to
+    back on one stream between two HIP events, after a read of a 1 GiB buffer
+    that evicts the cache from L2 and the MALL.  Algorithmic bytes are one
+    read of K and V (the kernel reads both twice: centroids, then distances)."""
+    C = w.capacity
+    log(f"bench: building the {w.name} cache at capacity ({w.units} units x {C} rows)")
+    k, v = synth.empty_cache(w, dev)
+    for s_ in range(w.num_seqs):
+        k[s_] = synth.block_rows(w, "k", s_, 0, 0, C, dev)
+        v[s_] = synth.block_rows(w, "v", s_, 0, 0, C, dev)
+    n = [C] * w.num_seqs
+    out = torch.empty((w.units, 5), dtype=torch.float64, device=dev)
+    flush_buf = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
+    for _ in range(args.warmup):
+        vd.vd_geometry(k, v, n, out)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    gpu_ms, wall_s, done = 0.0, 0.0, 0
+    while done < args.steps:   # segments of at most 20 passes, each after a flush
+        seg = min(20, args.steps - done)
+        flush_buf.sum()
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for _ in range(seg):
+            vd.vd_geometry(k, v, n, out)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall_s += time.perf_counter() - t0
+        gpu_ms += e0.elapsed_time(e1)
+        done += seg
+    alg = 2 * w.units * C * w.row_bytes
+    traffic = load_traffic(f"geometry_{w.name}")
+    us = gpu_ms / args.steps * 1e3
+    alg_gbps = alg / (us * 1e-6) / 1e9
+    log(f"bench: geometry {us:.2f} us per launch, {alg_gbps:.0f} GB/s algorithmic")
+    res = {
+        "metric": "geometry passes/s (sigma_K, sigma_V, mean distances, bos-cosim of every unit)",
+        "value": round(args.steps / wall_s, 2),
+        "unit": "passes/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall_s / args.steps * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if w.dtype == torch.bfloat16 else "f32",
+        "data": "synthetic (seeded generator; no model weights or datasets)",
+        "config": {"workload": f"{w.name} cache at capacity", "seqs": w.num_seqs,
+                   "layers": w.num_layers, "kv_heads": w.num_kv_heads,
+                   "head_dim": w.head_dim, "n": C},
+        "roofline": {"bound": "hbm", "achieved": round(alg_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(alg_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None if traffic is None else int(traffic),
+                     "traffic_over_alg": None if traffic is None else round(traffic / alg, 3),
+                     "kernel": f"geometry_kernel<bf16,{w.head_dim}>",
+                     "launch_us": round(us, 2), "alg_bytes_per_launch": alg,
+                     "bytes_read_per_launch": 2 * alg},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the oracle's geometry on the host ...")
+        res["cpu_baseline"] = cpu_geometry(w, k, v, args.cpu_seconds)
+    return res
+
+
+def cpu_geometry(w, k, v, budget_s):
+    """The oracle's geometry of units 0, 1, 2, ... of sequence 0 until about
+    budget_s seconds have passed, scaled to passes over every unit per second."""
+    import oracle
+    orc = oracle.load()
+    ku = to_np(k[0]).reshape(-1, w.capacity, w.head_dim)
+    vu = to_np(v[0]).reshape(-1, w.capacity, w.head_dim)
+    t0, done = time.perf_counter(), 0
+    while done < ku.shape[0] and time.perf_counter() - t0 < budget_s:
+        orc.geometry(ku[done], vu[done])
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": round(done / el / w.units, 4), "unit": "passes/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{done} of {w.units} units of {w.capacity} rows, one thread"}
+
+
 # ---------------------------------------------------------------- main
 
 def main():
@@ -304,6 +388,9 @@ def main():
                     help="the last two time decode steps (n = N + 1 in every sequence)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--geometry", action="store_true",
+                    help="time the geometry diagnostics (vd_geometry) over the workload's "
+                         "cache filled to capacity instead of the pass")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy three times (reference for the "
                          "HBM byte counters) and exit")
@@ -328,6 +415,9 @@ def main():
         return
     vd.load()
     w = synth.WORKLOADS[args.workload]()
+    if args.geometry:
+        print(json.dumps(geometry_bench(w, args, dev)), flush=True)
+        return
     decode = args.workload in ("decode_b16", "ragged_serving")
     if decode:
         log(f"bench: building the {w.name} decode cache ({w.units} units) ...")

@@ -146,6 +146,27 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid,
                         int32_t *pos, float *scores_out, uint8_t *keep_out,
                         void *workspace, size_t workspace_bytes, vd_stream stream);
 
+/*
+ * vd_geometry -- key and value geometry of every unit (Sec. 3.1, the spread
+ * of the distances to the centroid; Sec. 4, bos-cosim).
+ *   desc        K and V both required (desc->k non-NULL)
+ *   n_valid[s]  host; cached tokens of sequence s, 0 <= n <= capacity
+ *   out         device double [U][5], 8-byte aligned; per unit u
+ *               out[5u+0] sigma_K, out[5u+1] sigma_V: population standard
+ *                         deviation over the n rows of ||k_i - k_bar|| and
+ *                         ||v_i - v_bar|| (k_bar, v_bar: means of all n rows)
+ *               out[5u+2], out[5u+3]: the means of those distances
+ *               out[5u+4] cosine of k_0 and the mean of k_1 .. k_{n-1}
+ *                         (0 when n < 2 or either vector is zero)
+ *               all five are 0 for a unit with n = 0
+ * Centroids and every sum over rows are fp64; each distance is formed in
+ * fp32 (relative error within a few fp32 units in the last place).  Reads
+ * K and V twice, writes nothing else.  VD_ERR_INVALID_ARG for a NULL K,
+ * counts out of range or a NULL or misaligned out.
+ */
+vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double *out,
+                      vd_stream stream);
+
 /* Bytes of device workspace vd_evict_step needs for this descriptor (0 in this build). */
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);
 

@@ -235,6 +235,30 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const
     return VD_OK;
 }
 
+vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double *out,
+                      vd_stream stream) {
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if (!desc->k) return VD_ERR_INVALID_ARG;
+    if ((st = check_counts(desc, n_valid, nullptr)) != VD_OK) return st;
+    if (!out || !aligned(out, 8)) return VD_ERR_INVALID_ARG;
+    // fp64 reduction scratch, then the four centroid arrays (K hi, K lo, V hi, V lo)
+    const int64_t red_bytes = int64_t(vd::kWaves) * desc->head_dim * 8;
+    const int64_t ctr_bytes = int64_t(4) * desc->head_dim * 4;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
+        const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, nullptr);
+        p.geom_out = out;
+        p.off_keys = int32_t(sizeof(vd::LdsHead));
+        p.off_lists = int32_t(p.off_keys + red_bytes);
+        const size_t lds = size_t(p.off_lists + ctr_bytes);
+        st = launched(vd::launch_geometry(p, ns, desc->dtype, desc->head_dim, lds,
+                                          reinterpret_cast<hipStream_t>(stream)));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
+}
+
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc) {
     (void)desc;
     return 0;

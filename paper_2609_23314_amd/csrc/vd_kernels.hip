@@ -21,6 +21,10 @@
 //           slots at or above N, ascending; only those rows move; the same
 //           loop reads the evicted rows for the running-sum update
 //
+// A separate kernel, outside the pass, gives the key and value geometry of
+// each unit (spread of the distances to the centroid, Sec. 3.1; bos-cosim,
+// Sec. 4).
+//
 // The row stream is software-pipelined: chunk k of tile t+1 is requested as
 // soon as chunk k of tile t is used, and every lane loads unconditionally
 // (rows past the end are clamped to the last row and ignored).  No MFMA:
@@ -1152,6 +1156,219 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     }
 }
 
+// ---------------------------------------------------------------- geometry
+
+// Wave-wide fp64 sum by butterfly: every lane ends with the same bits.
+__device__ __forceinline__ double wave_sum_f64(double x) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+    return x;
+}
+
+// Element c of a row as fp32.
+template <int DT> __device__ __forceinline__ float row_elem(const char *row, int c) {
+    if constexpr (DT == 0)
+        return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(row)[c] << 16);
+    else
+        return reinterpret_cast<const float *>(row)[c];
+}
+
+// Geometry of one unit's keys and values (Sec. 3.1, and the bos-cosim of
+// Sec. 4): for K and for V, the mean distance of the n rows to their centroid
+// and the population standard deviation of those distances; and the cosine
+// between the first key and the mean of the other keys.  Two streams over the
+// rows: fp64 column sums of K and V, then one distance per row and tensor.  A
+// distance is taken in fp32 from the difference to the centroid held as an
+// fp32 pair (hi + lo), so that its error stays at fp32 rounding of the
+// distance however far the centroid lies from the origin; every sum over rows
+// is fp64, in a fixed order.  The first stream keeps the rows cacheable, the
+// second reads them once more, in reverse order and without retention.
+constexpr int kGeoRows = 2;  // rows per lane group in one tile of the geometry streams
+
+template <int DT, int D>
+__global__ void __launch_bounds__(NT) geometry_kernel(const UnitParams p) {
+    using S = Shape<DT, D>;
+    using E = Elem<DT>;
+    constexpr int kTile = S::GROUPS * kGeoRows;  // rows per tile
+    extern __shared__ __align__(16) unsigned char lds[];
+    LdsHead &H = *reinterpret_cast<LdsHead *>(lds);
+    double *red = reinterpret_cast<double *>(lds + p.off_keys);  // NW*D doubles
+    float *ctr = reinterpret_cast<float *>(lds + p.off_lists);   // K hi, K lo, V hi, V lo: D each
+
+    const int head = blockIdx.x, layer = blockIdx.y, sl = blockIdx.z;
+    const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
+    const int64_t u = (int64_t)p.unit0 + ul;
+    const int n = p.nN[2 * sl];
+    const int64_t off = (int64_t)sl * p.s_seq + (int64_t)layer * p.s_layer + (int64_t)head * p.s_head;
+    const char *kb = p.k + off;
+    const char *vb = p.v + off;
+    const uint32_t ss32 = p.s_slot;
+    double *out = p.geom_out + u * 5;
+    const int lane = lane_id(), w = wave_id();
+    const int cl = lane % S::LPR;
+    const int g = w * S::RPW + lane / S::LPR;  // this lane's row group
+    if (n == 0) {
+        if (threadIdx.x < 5) out[threadIdx.x] = 0.0;
+        return;
+    }
+
+    // Both streams keep one tile of 2 * kGeoRows 16-byte chunks in flight per
+    // lane (chunk j: row j/2 of the tile's kGeoRows rows of this lane's group;
+    // K for even j, V for odd j).  A chunk is refilled with the next tile's as soon
+    // as it is used; the refill's address depends on the used values, so the
+    // loads stay in order and each use waits for its own chunk only.  The
+    // tile after the last is requested too, with rows clamped into [0, n).
+    uint4 buf[2 * kGeoRows];
+    auto chunk_off = [&](int e0, int j, uint32_t z) __attribute__((always_inline)) {
+        return row_off(min(max(e0, 0) + (j >> 1) * S::GROUPS + g, n - 1), ss32, cl) + z;
+    };
+
+    // ---- centroids: fp64 column sums of all n rows ----
+    double ak[S::EPL], av[S::EPL];
+#pragma unroll
+    for (int i = 0; i < S::EPL; ++i) ak[i] = av[i] = 0.0;
+#pragma unroll
+    for (int j = 0; j < 2 * kGeoRows; ++j) {
+        buf[j] = *reinterpret_cast<const uint4 *>(((j & 1) ? vb : kb) + chunk_off(0, j, 0u));
+        __builtin_amdgcn_sched_barrier(0);  // issued in chunk order, as the loop reissues them
+    }
+    for (int e0 = 0; e0 < n; e0 += kTile) {
+#pragma unroll
+        for (int r = 0; r < kGeoRows; ++r) {
+            float x[S::EPL], y[S::EPL];
+            E::unpack(buf[2 * r], x);
+            E::unpack(buf[2 * r + 1], y);
+            const bool valid = e0 + r * S::GROUPS + g < n;  // selects, not a branch
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) {
+                ak[i] += valid ? (double)x[i] : 0.0;
+                av[i] += valid ? (double)y[i] : 0.0;
+            }
+            const uint32_t z = zero_after(x[0] + y[0]);
+            buf[2 * r] = *reinterpret_cast<const uint4 *>(kb + chunk_off(e0 + kTile, 2 * r, z));
+            buf[2 * r + 1] = *reinterpret_cast<const uint4 *>(vb + chunk_off(e0 + kTile, 2 * r + 1, z));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    }
+    const double sk = block_col_total<DT, D>(ak, red);
+    __syncthreads();  // every column total of K is read before red is refilled
+    const double sv = block_col_total<DT, D>(av, red);
+
+    // centroid pairs for the distance stream, and the bos-cosim terms:
+    // k_0 . m, |k_0|^2, |m|^2 with m the mean of keys 1 .. n-1
+    double bos_dot = 0.0, bos_k0 = 0.0, bos_m = 0.0;
+    if (threadIdx.x < D) {
+        const int t = threadIdx.x;
+        const double mk = sk / (double)n, mv = sv / (double)n;
+        const float kh = (float)mk, vh = (float)mv;
+        ctr[t] = kh;
+        ctr[D + t] = (float)(mk - (double)kh);
+        ctr[2 * D + t] = vh;
+        ctr[3 * D + t] = (float)(mv - (double)vh);
+        if (n >= 2) {
+            const double k0 = (double)row_elem<DT>(kb, t);
+            const double m = (sk - k0) / (double)(n - 1);
+            bos_dot = k0 * m;
+            bos_k0 = k0 * k0;
+            bos_m = m * m;
+        }
+    }
+    bos_dot = wave_sum_f64(bos_dot);
+    bos_k0 = wave_sum_f64(bos_k0);
+    bos_m = wave_sum_f64(bos_m);
+    if (lane == 0) {
+        H.old_sum[3 * w] = bos_dot;
+        H.old_sum[3 * w + 1] = bos_k0;
+        H.old_sum[3 * w + 2] = bos_m;
+    }
+    __syncthreads();
+
+    // ---- distances ----
+    float kh[S::EPL], kl[S::EPL], vh[S::EPL], vl[S::EPL];
+#pragma unroll
+    for (int i = 0; i < S::EPL; ++i) {
+        const int c = cl * S::EPL + i;
+        kh[i] = ctr[c];
+        kl[i] = ctr[D + c];
+        vh[i] = ctr[2 * D + c];
+        vl[i] = ctr[3 * D + c];
+    }
+    double s1k = 0.0, s2k = 0.0, s1v = 0.0, s2v = 0.0;
+    // last tile first: the rows the first stream read most recently are the
+    // likeliest still to be held in the caches
+    const int last = ((n - 1) / kTile) * kTile;
+#pragma unroll
+    for (int j = 0; j < 2 * kGeoRows; ++j) {
+        buf[j] = load_stream((j & 1) ? vb : kb, chunk_off(last, j, 0u));
+        __builtin_amdgcn_sched_barrier(0);
+    }
+    for (int e0 = last; e0 >= 0; e0 -= kTile) {
+#pragma unroll
+        for (int r = 0; r < kGeoRows; ++r) {
+            float x[S::EPL], y[S::EPL];
+            E::unpack(buf[2 * r], x);
+            E::unpack(buf[2 * r + 1], y);
+            float a = 0.f, b = 0.f;
+#pragma unroll
+            for (int i = 0; i < S::EPL; ++i) {
+                const float dx = (x[i] - kh[i]) - kl[i];
+                const float dy = (y[i] - vh[i]) - vl[i];
+                a = fmaf(dx, dx, a);
+                b = fmaf(dy, dy, b);
+            }
+            const uint32_t z = zero_after(a + b);
+            buf[2 * r] = load_stream(kb, chunk_off(e0 - kTile, 2 * r, z));
+            buf[2 * r + 1] = load_stream(vb, chunk_off(e0 - kTile, 2 * r + 1, z));
+            __builtin_amdgcn_sched_barrier(0);
+            const double dk = (double)score_sqrt(row_sum<S::LPR>(a));
+            const double dv = (double)score_sqrt(row_sum<S::LPR>(b));
+            const bool mine = cl == 0 && e0 + r * S::GROUPS + g < n;  // one lane per row
+            s1k += mine ? dk : 0.0;
+            s2k += mine ? dk * dk : 0.0;
+            s1v += mine ? dv : 0.0;
+            s2v += mine ? dv * dv : 0.0;
+        }
+    }
+    s1k = wave_sum_f64(s1k);
+    s2k = wave_sum_f64(s2k);
+    s1v = wave_sum_f64(s1v);
+    s2v = wave_sum_f64(s2v);
+    if (lane == 0) {  // red was last read before the barrier above
+        red[4 * w] = s1k;
+        red[4 * w + 1] = s2k;
+        red[4 * w + 2] = s1v;
+        red[4 * w + 3] = s2v;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double t[4] = {0.0, 0.0, 0.0, 0.0}, b[3] = {0.0, 0.0, 0.0};
+        for (int ww = 0; ww < NW; ++ww) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) t[j] += red[4 * ww + j];
+#pragma unroll
+            for (int j = 0; j < 3; ++j) b[j] += H.old_sum[3 * ww + j];
+        }
+        const double inv_n = 1.0 / (double)n;
+        const double muk = t[0] * inv_n, muv = t[2] * inv_n;
+        // population variance of the distances, E[d^2] - E[d]^2 in fp64
+        out[0] = sqrt(fmax(t[1] * inv_n - muk * muk, 0.0));
+        out[1] = sqrt(fmax(t[3] * inv_n - muv * muv, 0.0));
+        out[2] = muk;
+        out[3] = muv;
+        const double den = sqrt(b[1]) * sqrt(b[2]);
+        out[4] = den > 0.0 ? b[0] / den : 0.0;
+    }
+}
+
+template <int DT> void *geometry_kernel_for(int head_dim) {
+    switch (head_dim) {
+        case 64: return reinterpret_cast<void *>(&geometry_kernel<DT, 64>);
+        case 128: return reinterpret_cast<void *>(&geometry_kernel<DT, 128>);
+        case 256: return reinterpret_cast<void *>(&geometry_kernel<DT, 256>);
+    }
+    return nullptr;
+}
+
 template <int DT, int D> void *step_kernel_for(int variant) {
     switch (variant) {
         case 0: return reinterpret_cast<void *>(&step_kernel<DT, D, 0>);
@@ -1230,6 +1447,12 @@ __global__ void __launch_bounds__(256) stream_read_kernel(const u32x4 *buf, size
 hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream) {
     void *fn = dtype == 0 ? compact_kernel_for<0>(head_dim) : compact_kernel_for<1>(head_dim);
+    return launch(fn, num_seqs, lds_bytes, stream, p);
+}
+
+hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int head_dim,
+                           size_t lds_bytes, hipStream_t stream) {
+    void *fn = dtype == 0 ? geometry_kernel_for<0>(head_dim) : geometry_kernel_for<1>(head_dim);
     return launch(fn, num_seqs, lds_bytes, stream, p);
 }
 

@@ -58,6 +58,7 @@ struct UnitParams {
     uint8_t *keep;            // [U][capacity] or null (output of step/select)
     const uint8_t *keep_in;   // compact kernel input
     float *mean_out;          // [U][D] or null
+    double *geom_out;         // [U][5] (geometry kernel)
     int32_t nN[2 * kMaxSeqsPerLaunch];   // n and N of each sequence of the launch, interleaved
 };
 
@@ -68,6 +69,8 @@ hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
                          hipStream_t stream);
 hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream);
+hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int head_dim,
+                           size_t lds_bytes, hipStream_t stream);
 // Reads n16 16-byte words once over the whole GPU (a measurement aid).
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream);
 

@@ -24,7 +24,8 @@ VARIANTS = {"l2": 0, "dir": 1, "norm": 2}
 MAX_CAPACITY = 16384
 
 EXPORTS = ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step",
-           "vd_evict_step_workspace_size", "vd_status_string", "vd_stream_read")
+           "vd_evict_step_workspace_size", "vd_status_string", "vd_stream_read",
+           "vd_geometry")
 
 
 class VdError(RuntimeError):
@@ -71,6 +72,8 @@ def load():
     lib.vd_status_string.restype = ctypes.c_char_p
     lib.vd_stream_read.argtypes = [P, SZ, P, P]
     lib.vd_stream_read.restype = ctypes.c_int
+    lib.vd_geometry.argtypes = [D, P, P, P]
+    lib.vd_geometry.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -206,6 +209,23 @@ def vd_evict_step(k, v, n_valid, budget, variant="l2", running_sum=None, pos=Non
         ctypes.byref(desc), _ptr(n_h), _ptr(b_h), VARIANTS[variant], _ptr(running_sum),
         _ptr(pos), _ptr(scores_out), _ptr(keep_out), _ptr(workspace), ws_bytes,
         _stream(v.device, stream)))
+
+
+def vd_geometry(k, v, n_valid, out=None, *, stream=None):
+    """Key and value geometry of every unit (see ``vd_geometry`` in vd.h):
+    float64 [U, 5] = sigma_K, sigma_V, mean ||k - k_bar||, mean ||v - v_bar||,
+    bos-cosim."""
+    U = _units(v)
+    if k is None:
+        raise ValueError("vd_geometry needs k")
+    desc = cache_desc(v, k)
+    n_h = _host_i32(n_valid, v.shape[0], "n_valid")
+    if out is None:
+        out = torch.empty((U, 5), dtype=torch.float64, device=v.device)
+    _need(out, "out", torch.float64, U * 5, v.device)
+    _check("vd_geometry", load().vd_geometry(ctypes.byref(desc), _ptr(n_h), _ptr(out),
+                                             _stream(v.device, stream)))
+    return out
 
 
 def vd_stream_read(buf, sink, *, stream=None):

@@ -22,9 +22,9 @@ def declared_functions():
                                  text, flags=re.M)))
 
 
-def test_header_declares_the_four_calls():
+def test_header_declares_the_five_calls():
     names = declared_functions()
-    for f in ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step"):
+    for f in ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step", "vd_geometry"):
         assert f in names
     assert set(names) == set(vd.EXPORTS)
 
@@ -114,6 +114,24 @@ def test_stream_read_rejects_bad_arguments():
     assert lib.vd_stream_read(good, 24, good, None) == vd.VD_ERR_INVALID_ARG
     assert lib.vd_stream_read(good, 0, good, None) == vd.VD_ERR_INVALID_ARG
     assert lib.vd_stream_read(good, 16, None, None) == vd.VD_ERR_INVALID_ARG
+
+
+def test_geometry_rejects_bad_arguments():
+    lib = vd.load()
+    n_arr = (ctypes.c_int32 * 2)(5, 5)
+    out = ctypes.c_void_p(0x7F0000000000)
+    d = good_desc()
+    d.k = None                                   # K is required
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, out, None) == vd.VD_ERR_INVALID_ARG
+    d = good_desc()
+    assert lib.vd_geometry(ctypes.byref(d), None, out, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), (ctypes.c_int32 * 2)(101, 5), out,
+                           None) == vd.VD_ERR_INVALID_ARG            # n > capacity
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, ctypes.c_void_p(0x7F0000000004),
+                           None) == vd.VD_ERR_INVALID_ARG            # misaligned out
+    assert lib.vd_geometry(ctypes.byref(good_desc(head_dim=96)), n_arr, out,
+                           None) == vd.VD_ERR_UNSUPPORTED
 
 
 def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
