@@ -8,5 +8,5 @@ silent.
 """
 from .vdref import (  # noqa: F401
     BF16, F32, L2, DIR, NORM, VARIANTS,
-    Oracle, decode_elems, mean, score, select_topn, compact, evict_step, geometry, load,
+    Oracle, decode_elems, mean, score, select_topn, compact, evict_step, geometry, attention, load,
 )

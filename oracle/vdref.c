@@ -22,6 +22,10 @@
  *      evicted slots below N, ascending, receive the kept slots at or above N,
  *      ascending (the layout reading of "gather" used by this project).
  *
+ * Decode attention of one query row (Sec. 2.1, Eq. attention; grouped-query
+ * heads share a KV head): softmax of the scaled dot products with every cached
+ * key, applied to the values, in fp64.
+ *
  * Geometry diagnostics of one unit (Sec. 3.1 and the bos-cosim equation of
  * Sec. 4), from their definitions: sigma_X = std_i ||x_i - x_bar|| for X = K
  * and V (the population standard deviation over the n tokens), the mean of
@@ -378,5 +382,46 @@ int vdref_geometry(const void *k, const void *v, int dtype, int64_t n, int d,
         double denom = sqrt(n0) * sqrt(nm);
         out[4] = denom > 0.0 ? dot / denom : 0.0;
     }
+    return VDREF_OK;
+}
+
+/* ---- decode attention (Sec. 2.1, Eq. attention) ------------------------ */
+
+/*
+ * One query row of one head against rows 0 .. n-1 of its KV head:
+ * out = sum_j softmax_j(scale * q . k_j) v_j.  For the newest token the causal
+ * mask keeps every cached row, so it does not appear.  The largest logit is
+ * subtracted before exponentiation (softmax does not change under a common
+ * shift of its arguments).
+ */
+int vdref_attention(const double *q, const void *k, const void *v, int dtype, int64_t n,
+                    int d, int64_t row_stride, double scale, double *out)
+{
+    if (n <= 0 || d <= 0 || !q || !k || !v || !out)
+        return VDREF_BAD_ARG;
+    double *w = (double *)malloc(sizeof(double) * (size_t)n);
+    if (!w)
+        return VDREF_BAD_ARG;
+    double top = -INFINITY;
+    for (int64_t j = 0; j < n; ++j) {
+        double dot = 0.0;
+        for (int c = 0; c < d; ++c)
+            dot += q[c] * get_elem(k, dtype, j * row_stride + c);
+        w[j] = scale * dot;
+        if (w[j] > top)
+            top = w[j];
+    }
+    double den = 0.0;
+    for (int64_t j = 0; j < n; ++j) {
+        w[j] = exp(w[j] - top);
+        den += w[j];
+    }
+    for (int c = 0; c < d; ++c) {
+        double acc = 0.0;
+        for (int64_t j = 0; j < n; ++j)
+            acc += w[j] * get_elem(v, dtype, j * row_stride + c);
+        out[c] = acc / den;
+    }
+    free(w);
     return VDREF_OK;
 }

@@ -60,8 +60,9 @@ class Oracle:
         lib.vdref_evict_step.argtypes = [_p, _p, _i32, _i64, _i64, _i32, _p, _p, _i32,
                                          _p, _p, _p, _p, _i32]
         lib.vdref_geometry.argtypes = [_p, _p, _i32, _i64, _i32, _i64, _p]
+        lib.vdref_attention.argtypes = [_p, _p, _p, _i32, _i64, _i32, _i64, ctypes.c_double, _p]
         for f in ("vdref_mean", "vdref_score", "vdref_select_topn", "vdref_compact",
-                  "vdref_evict_step", "vdref_geometry"):
+                  "vdref_evict_step", "vdref_geometry", "vdref_attention"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = path
@@ -123,6 +124,20 @@ class Oracle:
         out = np.empty(5, np.float64)
         if self.lib.vdref_geometry(_ptr(k), _ptr(v), _dtype_tag(v), n, d, d, _ptr(out)):
             raise ValueError("vdref_geometry rejected its arguments")
+        return out
+
+    def attention(self, q: np.ndarray, k: np.ndarray, v: np.ndarray, scale: float) -> np.ndarray:
+        """softmax(scale * q . k_j) weighted sum of the rows v_j: q [d] (any
+        float dtype, taken as fp64), k and v [n, d]; returns float64 [d]."""
+        k, v = np.ascontiguousarray(k), np.ascontiguousarray(v)
+        q = np.ascontiguousarray(q, dtype=np.float64)
+        if k.shape != v.shape or k.dtype != v.dtype or q.shape != (v.shape[1],):
+            raise ValueError("q [d], k and v [n, d] of one dtype")
+        n, d = v.shape
+        out = np.empty(d, np.float64)
+        if self.lib.vdref_attention(_ptr(q), _ptr(k), _ptr(v), _dtype_tag(v), n, d, d,
+                                    float(scale), _ptr(out)):
+            raise ValueError("vdref_attention rejected its arguments")
         return out
 
     def evict_step(self, k, v, n_unit, N_unit, variant="l2", pos=None, nthreads=0):
@@ -193,3 +208,7 @@ def evict_step(k, v, n_unit, N_unit, variant="l2", pos=None, nthreads=0):
 
 def geometry(k, v):
     return load().geometry(k, v)
+
+
+def attention(q, k, v, scale):
+    return load().attention(q, k, v, scale)

@@ -16,6 +16,9 @@ Pins and what they fix:
   decoding            bf16 and fp32 element values against torch's conversion
   geometry            sigma_K / sigma_V / bos-cosim (Sec. 3.1, Sec. 4): hand values,
                       closed forms, invariances and special cases
+  attention           decode attention (Sec. 2.1, Eq. attention): zero query = mean,
+                      one row, hand weights 1/4 and 3/4, scale, overflow-free one-hot,
+                      key shift, permutation, bf16
 """
 import itertools
 import json
@@ -380,11 +383,56 @@ def check_geometry(orc):
     assert _rel_close(orc.geometry(kb, vb), orc.geometry(kf, vf), 1e-12, 1e-15)
 
 
+def check_attention(orc):
+    """Decode attention o = sum_j softmax_j(scale * q . k_j) v_j (Sec. 2.1,
+    Eq. attention) against hand values and properties that fix it."""
+    rng = np.random.default_rng(41)
+    k = _f32(rng.standard_normal((30, 8)))
+    v = _f32(rng.standard_normal((30, 8)) * 2.0)
+    v64 = v.astype(np.float64)
+    # a zero query weighs every row alike: the output is the plain mean of the rows
+    o = orc.attention(np.zeros(8), k, v, 0.35)
+    assert _rel_close(o, v64.sum(axis=0) / 30.0, 1e-12, 1e-14), o
+    # one row: the output is that row
+    assert np.array_equal(orc.attention(rng.standard_normal(8), k[:1], v[:1], 0.35), v64[0])
+    # two rows with logits 0 and ln 3 weigh 1/4 and 3/4: (4, -8)/4 + 3 (0, 8)/4 = (1, 4)
+    o = orc.attention(np.array([np.log(3.0), 5.0]), _f32([[0, 0], [1, 0]]),
+                      _f32([[4, -8], [0, 8]]), 1.0)
+    assert _rel_close(o, [1.0, 4.0], 1e-12, 1e-12), o
+    # the scale multiplies the logits
+    q = rng.standard_normal(8)
+    a = orc.attention(q, k, v, 0.7)
+    assert _rel_close(a, orc.attention(0.7 * q, k, v, 1.0), 1e-12, 1e-14)
+    assert not _rel_close(a, orc.attention(q, k, v, 1.0), 1e-6)
+    # one logit 1000 above the others: exactly that row, with no overflow
+    big = np.zeros(8)
+    big[0] = 1000.0
+    kk = np.zeros((5, 8), np.float32)
+    kk[2, 0] = 1.0
+    assert np.array_equal(orc.attention(big, kk, v[:5], 1.0), v64[2])
+    # the same shift of every key moves every logit alike: no change (integer
+    # keys, so that the shifted keys are exact)
+    ki = _f32(rng.integers(-4, 5, (30, 8)))
+    ks = _f32(ki + rng.integers(-3, 4, 8))
+    assert _rel_close(orc.attention(q, ks, v, 0.3), orc.attention(q, ki, v, 0.3), 1e-11, 1e-13)
+    # rows permuted together with their values: no change
+    perm = rng.permutation(30)
+    assert _rel_close(orc.attention(q, k[perm], v[perm], 0.5), orc.attention(q, k, v, 0.5),
+                      1e-12, 1e-14)
+    # bf16 rows give the output of their fp32 values
+    kb = (k.view(np.uint32) >> 16).astype(np.uint16)
+    vb = (v.view(np.uint32) >> 16).astype(np.uint16)
+    kf = _f32((kb.astype(np.uint32) << 16).view(np.float32))
+    vf = _f32((vb.astype(np.uint32) << 16).view(np.float32))
+    assert _rel_close(orc.attention(q, kb, vb, 0.5), orc.attention(q, kf, vf, 0.5), 1e-12, 1e-15)
+
+
 ALL_CHECKS = [
     check_decode, check_mean_library, check_worked_examples,
     check_minimal_disturbance, check_law_of_cosines, check_dirichlet,
     check_invariances, check_select_vs_sort, check_select_bruteforce,
     check_select_special, check_compact, check_evict_step_batch, check_geometry,
+    check_attention,
 ]
 
 

@@ -51,6 +51,13 @@ MUTANTS = [
      "for (int64_t i = 0; i < n; ++i)\n                m +="),
     ("sigma_k_of_v", "dispersion(k, dtype, n, d, row_stride, &out[2], &out[0]);",
      "dispersion(v, dtype, n, d, row_stride, &out[2], &out[0]);"),
+    ("attn_no_max_shift", "w[j] = exp(w[j] - top);", "w[j] = exp(w[j]);"),
+    ("attn_ignores_scale", "w[j] = scale * dot;", "w[j] = dot;"),
+    ("attn_divides_by_n", "out[c] = acc / den;", "out[c] = acc / (double)n;"),
+    ("attn_same_key_for_all", "dot += q[c] * get_elem(k, dtype, j * row_stride + c);",
+     "dot += q[c] * get_elem(k, dtype, c);"),
+    ("attn_values_from_keys", "acc += w[j] * get_elem(v, dtype, j * row_stride + c);",
+     "acc += w[j] * get_elem(k, dtype, j * row_stride + c);"),
 ]
 
 
