@@ -358,6 +358,116 @@ def geometry_bench(w, args, dev):
     return res
 
 
+def decode_attention_bench(args, dev):
+    """Decode steps of the decode_b16 workload with the attention of the newest
+    token fused to its eviction: per step one vd_decode_attention_evict call
+    per layer (the layers of a model run one after another), each over the
+    layer's 16 x 8 units at n = N + 1 = 4097, with that layer's running sum.
+    The calls are replayed in place (after a call slot N still holds a row, so
+    n = N + 1 is again a well-formed step).  Algorithmic bytes per call: one
+    read of K and V, the moved rows (K and V read and written), the running
+    sum read and written, q read and the output written."""
+    w = synth.decode()
+    S, L, H, D = w.num_seqs, w.num_layers, w.num_kv_heads, w.head_dim
+    Hq, N = w.num_q_heads, w.budget[0]
+    log(f"bench: building the {w.name} decode cache ({w.units} units)")
+    k, v, rs, n = decode_state(w, dev)
+    rs_l = [rs.view(S, L, H, D + 1)[:, l].reshape(S * H, D + 1).contiguous() for l in range(L)]
+    g = torch.Generator(device=dev)
+    g.manual_seed(1234)
+    q_l = [torch.randn((S, 1, Hq, D), generator=g, device=dev) for _ in range(L)]
+    out = torch.empty((S, 1, Hq, D), dtype=torch.float32, device=dev)
+    kv_l = [(k[:, l:l + 1], v[:, l:l + 1]) for l in range(L)]
+    ws = torch.zeros(vd.vd_decode_attention_workspace_size(kv_l[0][0], kv_l[0][1], Hq),
+                     dtype=torch.uint8, device=dev)
+    # moved rows of one call (untimed, on copies)
+    pos = torch.arange(w.capacity, dtype=torch.int32, device=dev).repeat(S * H, 1).contiguous()
+    vd.vd_decode_attention_evict(kv_l[0][0].clone(), kv_l[0][1].clone(), q_l[0], n, w.budget,
+                                 rs_l[0].clone(), pos=pos, out=out, workspace=ws)
+    movers = int((pos[:, :N] != torch.arange(N, dtype=torch.int32, device=dev)).any(dim=1).sum())
+
+    def step():
+        for l in range(L):
+            vd.vd_decode_attention_evict(kv_l[l][0], kv_l[l][1], q_l[l], n, w.budget, rs_l[l],
+                                         out=out, workspace=ws)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream(dev)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = e0.elapsed_time(e1)
+    calls = args.steps * L
+    us_call = ms * 1e3 / calls
+    units = S * H
+    alg = (2 * units * (N + 1) * w.row_bytes + movers * 4 * w.row_bytes
+           + units * (D + 1) * 16 + S * Hq * D * 8)
+    gbps = alg / (us_call * 1e-6) / 1e9
+    traffic = load_traffic("decode_attention_decode_b16")
+    log(f"bench: {us_call:.2f} us per layer call, {gbps:.0f} GB/s algorithmic, {movers} movers of {units}")
+    # the eviction pass alone over all layers (vd_evict_step), for context
+    _, ev_ms = time_in_place(w, k, v, rs, n, 10, 2, dev)
+    res = {
+        "metric": "decode steps/s (attention of the newest token fused to its eviction, all layers)",
+        "value": round(args.steps / wall, 2),
+        "unit": "steps/s",
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded generator; no model weights or datasets)",
+        "config": {"workload": "decode_b16 decode step, one call per layer", "seqs": S,
+                   "layers": L, "kv_heads": H, "q_heads": Hq, "head_dim": D, "budget": N,
+                   "n": N + 1},
+        "roofline": {"bound": "hbm", "achieved": round(gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": None if traffic is None else int(traffic),
+                     "traffic_over_alg": None if traffic is None else round(traffic / alg, 3),
+                     "kernel": "attn_split_kernel<bf16,128,4> + attn_combine_kernel (one call)",
+                     "launch_us": round(us_call, 2), "alg_bytes_per_launch": alg},
+        "evict_pass_alone_us": round(ev_ms * 1e3 / 10, 2),
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the oracle on the host ...")
+        res["cpu_baseline"] = cpu_decode_attention(w, kv_l[0][0], kv_l[0][1], q_l[0], rs_l[0],
+                                                   n, args.cpu_seconds)
+    return res
+
+
+def cpu_decode_attention(w, k, v, q, rs, n, budget_s):
+    """The oracle's attention (every query head) and eviction for units of one
+    layer, one at a time, for about budget_s seconds; scaled to whole steps
+    (all layers) per second."""
+    import oracle
+    orc = oracle.load()
+    S, H, D, C = w.num_seqs, w.num_kv_heads, w.head_dim, w.capacity
+    G = w.num_q_heads // H
+    kn = to_np(k).reshape(S * H, C, D)
+    vn = to_np(v).reshape(S * H, C, D)
+    qn = q.cpu().numpy().astype(np.float64).reshape(S * H, G, D)
+    m = n[0]
+    t0, done = time.perf_counter(), 0
+    while done < S * H and time.perf_counter() - t0 < budget_s:
+        for g in range(G):
+            orc.attention(qn[done, g], kn[done, :m], vn[done, :m], D ** -0.5)
+        kc, vc = kn[done:done + 1].copy(), vn[done:done + 1].copy()
+        orc.evict_step(kc, vc, np.array([m], np.int32), np.array([w.budget[0]], np.int32), "l2")
+        done += 1
+    el = time.perf_counter() - t0
+    return {"value": round(done / el / w.units, 4), "unit": "steps/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{done} units of one layer (attention of {G} heads and eviction, n={m}), "
+                      f"one thread, scaled to a step of {w.units} units"}
+
+
 def cpu_geometry(w, k, v, budget_s):
     """The oracle's geometry of units 0, 1, 2, ... of sequence 0 until about
     budget_s seconds have passed, scaled to passes over every unit per second."""
@@ -391,6 +501,9 @@ def main():
     ap.add_argument("--geometry", action="store_true",
                     help="time the geometry diagnostics (vd_geometry) over the workload's "
                          "cache filled to capacity instead of the pass")
+    ap.add_argument("--decode-attention", action="store_true",
+                    help="time decode steps of the decode_b16 workload with attention fused "
+                         "to the eviction (vd_decode_attention_evict), one call per layer")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain 1 GiB device copy three times (reference for the "
                          "HBM byte counters) and exit")
@@ -417,6 +530,9 @@ def main():
     w = synth.WORKLOADS[args.workload]()
     if args.geometry:
         print(json.dumps(geometry_bench(w, args, dev)), flush=True)
+        return
+    if args.decode_attention:
+        print(json.dumps(decode_attention_bench(args, dev)), flush=True)
         return
     decode = args.workload in ("decode_b16", "ragged_serving")
     if decode:

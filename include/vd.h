@@ -167,6 +167,48 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid,
 vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double *out,
                       vd_stream stream);
 
+/*
+ * vd_decode_attention_evict -- one decode step of every sequence, fused with
+ * its eviction: attention of the newest token over the n cached rows (Sec.
+ * 2.1, Eq. attention; B = 1 in Eq. block_processing), then, where n = N + 1,
+ * the eviction of the row with the lowest L2 score (Sec. 3.2, Eq. vd; Sec.
+ * 2.1, Eq. eviction) scored in the same pass over V.
+ *   desc          K and V both required; num_q_heads = G * num_kv_heads with
+ *                 G in {1, 2, 4}; query head h*G + g uses KV head h
+ *   q             device float [S][L][num_q_heads][head_dim], contiguous: the
+ *                 newest token's query rows
+ *   scale         softmax scale (1/sqrt(head_dim) in the paper), finite
+ *   n_valid[s]    host; cached tokens, the newest included; n <= budget + 1
+ *   budget[s]     host; N >= 1
+ *   running_sum   device double [U][head_dim + 1], required: the column sums
+ *                 of the rows it covers, then their count (as vd_evict_step);
+ *                 on return it covers the rows left.  Rows it does not cover
+ *                 are read by every workgroup of the unit, so it should cover
+ *                 all but the newest row.
+ *   pos           device int32 [U][capacity] or NULL; moved with the rows
+ *   out           device float [S][L][num_q_heads][head_dim]: the attention
+ *                 output of every query row (0 for a sequence with n = 0)
+ *   workspace     device, 16-byte aligned, at least
+ *                 vd_decode_attention_workspace_size(desc) bytes; calls that
+ *                 share a workspace must not overlap
+ * A unit's rows are split over several workgroups; a second kernel merges
+ * them, so the attention reads every row before anything moves.  Eviction:
+ * the row
+ * with the lowest score goes, the highest slot among equal lowest scores; if
+ * it lies below N, row N takes its slot (K, V and pos).  Scores and softmax are
+ * fp32 (log2-domain exponentials), the mean and the running sum fp64.
+ * VD_ERR_UNSUPPORTED for n > budget + 1 or another G; VD_ERR_WORKSPACE for a
+ * missing or short workspace; VD_ERR_INVALID_ARG as the other calls.
+ */
+vd_status vd_decode_attention_evict(const vd_cache_desc *desc, const float *q, float scale,
+                                    const int32_t *n_valid, const int32_t *budget,
+                                    double *running_sum, int32_t *pos, float *out,
+                                    void *workspace, size_t workspace_bytes, vd_stream stream);
+
+/* Bytes of device workspace vd_decode_attention_evict needs for this
+ * descriptor (0 for an invalid descriptor). */
+size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc);
+
 /* Bytes of device workspace vd_evict_step needs for this descriptor (0 in this build). */
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);
 

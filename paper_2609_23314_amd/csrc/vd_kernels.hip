@@ -1369,6 +1369,318 @@ template <int DT> void *geometry_kernel_for(int head_dim) {
     return nullptr;
 }
 
+// ---------------------------------------------------------------- decode attention
+
+// One decode step of the newest token of every sequence fused with its
+// eviction (Sec. 2.1, Eq. attention and Eq. eviction, with B = 1 in Eq.
+// block_processing): the query rows of the G query heads that share a KV head
+// attend to all n cached rows, and the same stream over V scores every row
+// against the mean that the running sum gives (Sec. 3.2, Eq. vd), so that the
+// eviction needs no V read of its own.  A unit's rows are split over several
+// workgroups (split kernel); a second kernel merges the splits, evicts the row
+// with the lowest score when n = N + 1, moves the newest row into its slot and
+// updates the running sum.  (A merge by the last split to finish needs a
+// device-scope release per workgroup, which writes back the XCD's L2 and was
+// measured several times slower.)
+//
+// Softmax runs in log2 units (the query is pre-scaled by scale * log2(e)) with
+// a running maximum: every lane group keeps, per head, the largest logit so
+// far, the sum of 2^(z - max) and the weighted sum of its value columns,
+// rescaled when the maximum grows; two rows are taken at a time.
+constexpr int kAttnWaves = kAttnThreads / 64;
+constexpr float kNoLogit = -1.0e30f;  // below every logit, finite (2^(kNoLogit - z) = 0)
+constexpr int kAttnRows = 2;           // rows per lane group in one tile of the split kernel
+
+template <int DT, int D> struct AttnShape {
+    static constexpr int EPL = Elem<DT>::EPL;
+    static constexpr int ROWB = D * Elem<DT>::BYTES;
+    static constexpr int LPR = ROWB / 16;
+    static constexpr int RPW = 64 / LPR;
+    static constexpr int GROUPS = kAttnWaves * RPW;   // row groups of a workgroup
+    static constexpr int TILE = kAttnRows * GROUPS;   // rows per tile
+};
+
+// fp64 mean of a unit's n rows from the running sum (count rows) plus the rows
+// [count, n) read here, as fp32, into mean[0 .. D); thread t < D takes column t.
+template <int DT, int D>
+__device__ __forceinline__ void attn_mean(const double *st, const char *vb, uint32_t ss, int n,
+                                          int count, float *mean) {
+    if (threadIdx.x < D) {
+        const int t = threadIdx.x;
+        double f = 0.0;
+        for (int r = count; r < n; ++r) f += (double)row_elem<DT>(vb + (size_t)r * ss, t);
+        const double old = count > 0 ? st[t] : 0.0;
+        mean[t] = (float)((old + f) / (double)n);
+    }
+}
+
+__device__ __forceinline__ int state_count(const double *st, int n) {
+    const double c = st[0];
+    return (c >= 0.0 && c <= (double)n && c == (double)(int)c) ? (int)c : 0;
+}
+
+template <int DT, int D, int G>
+__global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitParams p) {
+    using A = AttnShape<DT, D>;
+    using E = Elem<DT>;
+    constexpr int EPL = A::EPL, LPR = A::LPR, GROUPS = A::GROUPS;
+    extern __shared__ __align__(16) unsigned char lds[];
+    float *mean = reinterpret_cast<float *>(lds);                          // D
+    float *gmax = mean + D;                                                // GROUPS * G
+    float *gsum = gmax + GROUPS * G;                                       // GROUPS * G
+    unsigned long long *wmin = reinterpret_cast<unsigned long long *>(gsum + GROUPS * G);  // kAttnWaves
+    float *red = reinterpret_cast<float *>(wmin + kAttnWaves);             // G * GROUPS * D
+
+    const int sp = blockIdx.x, head = blockIdx.y;
+    const int sl = blockIdx.z / p.num_layers, layer = blockIdx.z % p.num_layers;
+    const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
+    const int64_t u = (int64_t)p.unit0 + ul;
+    const int n = p.nN[2 * sl];
+    const int64_t off = (int64_t)sl * p.s_seq + (int64_t)layer * p.s_layer + (int64_t)head * p.s_head;
+    const char *kb = p.k + off;
+    const char *vb = p.v + off;
+    const uint32_t ss32 = p.s_slot;
+    const double *st = p.running_sum + u * (D + 1);
+    const int lane = lane_id(), w = wave_id();
+    const int cl = lane % LPR;
+    const int grp = w * A::RPW + lane / LPR;
+    const int r0 = sp * p.split_rows;
+    const int r1 = min(n, r0 + p.split_rows);
+    const int64_t wsi = u * p.splits + sp;
+
+    if (r1 > r0) attn_mean<DT, D>(st, vb, ss32, n, state_count(st + D, n), mean);
+    // this lane's columns of the G query rows, pre-scaled
+    float qs[G][EPL];
+    const float *qrow = p.q + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
+#pragma unroll
+    for (int g = 0; g < G; ++g)
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) qs[g][i] = qrow[g * D + cl * EPL + i] * p.qscale;
+    __syncthreads();
+    float mv[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) mv[i] = mean[cl * EPL + i];
+
+    float mx[G], ls[G], acc[G][EPL];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        mx[g] = kNoLogit;
+        ls[g] = 0.f;
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) acc[g][i] = 0.f;
+    }
+    unsigned long long amin = ~0ull;
+
+    if (r1 > r0) {
+        // chunk j of a tile: row j/2 of this group's kAttnRows rows, K for even j, V for odd
+        uint4 buf[2 * kAttnRows];
+        auto chunk_off = [&](int e0, int j, uint32_t z) __attribute__((always_inline)) {
+            return row_off(min(e0 + (j >> 1) * GROUPS + grp, r1 - 1), ss32, cl) + z;
+        };
+#pragma unroll
+        for (int j = 0; j < 2 * kAttnRows; ++j) {
+            buf[j] = load_stream((j & 1) ? vb : kb, chunk_off(r0, j, 0u));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        for (int e0 = r0; e0 < r1; e0 += A::TILE) {
+            float z[kAttnRows][G], vx[kAttnRows][EPL];
+            bool valid[kAttnRows];
+#pragma unroll
+            for (int r = 0; r < kAttnRows; ++r) {
+                float kx[EPL];
+                E::unpack(buf[2 * r], kx);
+                E::unpack(buf[2 * r + 1], vx[r]);
+                const int e = e0 + r * GROUPS + grp;
+                valid[r] = e < r1;
+                float a[G];
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    a[g] = 0.f;
+#pragma unroll
+                    for (int i = 0; i < EPL; ++i) a[g] = fmaf(qs[g][i], kx[i], a[g]);
+                }
+                float b = 0.f;
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) {
+                    const float t = vx[r][i] - mv[i];
+                    b = fmaf(t, t, b);
+                }
+                // refill both chunks of this row with the next tile's
+                const uint32_t zz = zero_after(a[0] + b);
+                buf[2 * r] = load_stream(kb, chunk_off(e0 + A::TILE, 2 * r, zz));
+                buf[2 * r + 1] = load_stream(vb, chunk_off(e0 + A::TILE, 2 * r + 1, zz));
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int g = 0; g < G; ++g) z[r][g] = valid[r] ? row_sum<LPR>(a[g]) : kNoLogit;
+                // L2 score of the value row (Sec. 3.2, Eq. vd) and its key
+                const uint32_t key = score_key(score_sqrt(row_sum<LPR>(b)));
+                const unsigned long long pk = ((unsigned long long)key << 32) | (uint32_t)~(uint32_t)e;
+                amin = valid[r] && pk < amin ? pk : amin;
+            }
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                float mn = mx[g];
+#pragma unroll
+                for (int r = 0; r < kAttnRows; ++r) mn = fmaxf(mn, z[r][g]);
+                float w[kAttnRows], ws = 0.f;
+#pragma unroll
+                for (int r = 0; r < kAttnRows; ++r) {
+                    w[r] = valid[r] ? __builtin_amdgcn_exp2f(z[r][g] - mn) : 0.f;
+                    ws += w[r];
+                }
+                const float c = __builtin_amdgcn_exp2f(mx[g] - mn);
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) {
+                    float x = acc[g][i] * c;
+#pragma unroll
+                    for (int r = 0; r < kAttnRows; ++r) x = fmaf(w[r], vx[r][i], x);
+                    acc[g][i] = x;
+                }
+                ls[g] = fmaf(ls[g], c, ws);
+                mx[g] = mn;
+            }
+        }
+    }
+
+    // merge the row groups: per head the largest logit, then the rescaled sums
+    // in a fixed order
+    if (cl == 0)
+#pragma unroll
+        for (int g = 0; g < G; ++g) gmax[grp * G + g] = mx[g];
+    amin = wave_min_u64(amin);
+    if (lane == 0) wmin[w] = amin;
+    __syncthreads();
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        float top = kNoLogit;
+        for (int q = 0; q < GROUPS; ++q) top = fmaxf(top, gmax[q * G + g]);
+        const float f = __builtin_amdgcn_exp2f(mx[g] - top);
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) red[(g * GROUPS + grp) * D + cl * EPL + i] = acc[g][i] * f;
+        if (cl == 0) gsum[grp * G + g] = ls[g] * f;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < G * D; idx += kAttnThreads) {
+        const int g = idx / D, c = idx % D;
+        float s = 0.f;
+        for (int q = 0; q < GROUPS; ++q) s += red[(g * GROUPS + q) * D + c];
+        p.ws_acc[(wsi * G + g) * D + c] = s;
+    }
+    if (threadIdx.x < G) {
+        const int g = threadIdx.x;
+        float top = kNoLogit, l = 0.f;
+        for (int q = 0; q < GROUPS; ++q) top = fmaxf(top, gmax[q * G + g]);
+        for (int q = 0; q < GROUPS; ++q) l += gsum[q * G + g];
+        p.ws_ml[(wsi * G + g) * 2] = top;
+        p.ws_ml[(wsi * G + g) * 2 + 1] = l;
+    }
+    if (threadIdx.x == 0) {
+        unsigned long long m = ~0ull;
+        for (int q = 0; q < kAttnWaves; ++q) m = wmin[q] < m ? wmin[q] : m;
+        p.ws_amin[wsi] = m;
+    }
+}
+
+// Merges a unit's splits into the attention output of its G query rows, then
+// evicts (n = N + 1: the row with the lowest score, the highest slot among
+// equal lowest scores; Sec. 2.1, Eq. eviction), moves row N into the freed
+// slot below N (slot reuse) and updates the running sum.  Launched after the
+// split kernel, so every row has been read before anything moves.  The loads
+// that do not depend on the evicted slot (state, rows not in the state,
+// partials, argmin words) all go out first.
+template <int DT, int D, int G>
+__global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitParams p) {
+    using A = AttnShape<DT, D>;
+    constexpr int kOut = (G * D + kAttnThreads - 1) / kAttnThreads;  // outputs per thread
+    __shared__ int jev;
+    const int head = blockIdx.x;
+    const int sl = blockIdx.y / p.num_layers, layer = blockIdx.y % p.num_layers;
+    const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
+    const int64_t u = (int64_t)p.unit0 + ul;
+    const int n = p.nN[2 * sl], N = p.nN[2 * sl + 1];
+    const int64_t off = (int64_t)sl * p.s_seq + (int64_t)layer * p.s_layer + (int64_t)head * p.s_head;
+    char *kb = p.k + off;
+    char *vb = p.v + off;
+    const uint32_t ss32 = p.s_slot;
+    double *st = p.running_sum + u * (D + 1);
+    const int S = p.splits;
+    const bool evict = n > N;  // the host admits n <= N + 1 only
+    // state and the rows it does not cover
+    const int count = state_count(st + D, n);
+    double part = 0.0;
+    if (threadIdx.x < D) {
+        const int t = threadIdx.x;
+        double f = 0.0;
+        for (int r = count; r < n; ++r) f += (double)row_elem<DT>(vb + (size_t)r * ss32, t);
+        part = (count > 0 ? st[t] : 0.0) + f;
+    }
+    // the evicted slot
+    if (threadIdx.x < 64) {
+        unsigned long long m = ~0ull;
+        for (int s = threadIdx.x; s < S; s += 64) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
+        m = wave_min_u64(m);
+        if (threadIdx.x == 0) jev = evict ? (int)~(uint32_t)m : -1;
+    }
+    // outputs
+    float *orow = p.attn_out + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
+    const float *ml = p.ws_ml + u * S * G * 2;
+    const float *pa = p.ws_acc + u * S * G * D;
+#pragma unroll
+    for (int o = 0; o < kOut; ++o) {
+        const int idx = threadIdx.x + o * kAttnThreads;
+        if (idx < G * D) {
+            const int g = idx / D, c = idx % D;
+            float top = kNoLogit;
+            for (int s = 0; s < S; ++s) top = fmaxf(top, ml[(s * G + g) * 2]);
+            float num = 0.f, den = 0.f;
+#pragma unroll 4
+            for (int s = 0; s < S; ++s) {
+                const float f = __builtin_amdgcn_exp2f(ml[(s * G + g) * 2] - top);
+                num = fmaf(pa[(s * G + g) * D + c], f, num);
+                den = fmaf(ml[(s * G + g) * 2 + 1], f, den);
+            }
+            orow[g * D + c] = n > 0 ? num / den : 0.f;
+        }
+    }
+    __syncthreads();
+    const int j = jev;
+    // running sum minus the evicted row, read before the move below
+    if (threadIdx.x < D) {
+        const double ev = j >= 0 ? (double)row_elem<DT>(vb + (size_t)j * ss32, threadIdx.x) : 0.0;
+        st[threadIdx.x] = part - ev;
+    }
+    if (threadIdx.x == 0) st[D] = (double)(evict ? N : n);
+    __syncthreads();
+    if (j >= 0 && j < N) {  // slot reuse: the newest kept row N fills the hole
+        for (int c = threadIdx.x; c < 2 * A::LPR; c += kAttnThreads) {
+            char *base = c < A::LPR ? kb : vb;
+            const int ch = c % A::LPR;
+            store_stream(base, row_off(j, ss32, ch), load_stream(base, row_off(N, ss32, ch)));
+        }
+        if (p.pos && threadIdx.x == 0) p.pos[u * p.capacity + j] = p.pos[u * p.capacity + N];
+    }
+}
+
+template <int DT, int D> void *attn_kernel_for(int group, bool combine) {
+    switch (group) {
+        case 1: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 1>)
+                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 1>);
+        case 2: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 2>)
+                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 2>);
+        case 4: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 4>)
+                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 4>);
+    }
+    return nullptr;
+}
+template <int DT> void *attn_kernel_for(int head_dim, int group, bool combine) {
+    switch (head_dim) {
+        case 64: return attn_kernel_for<DT, 64>(group, combine);
+        case 128: return attn_kernel_for<DT, 128>(group, combine);
+        case 256: return attn_kernel_for<DT, 256>(group, combine);
+    }
+    return nullptr;
+}
+
 template <int DT, int D> void *step_kernel_for(int variant) {
     switch (variant) {
         case 0: return reinterpret_cast<void *>(&step_kernel<DT, D, 0>);
@@ -1454,6 +1766,19 @@ hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int hea
                            size_t lds_bytes, hipStream_t stream) {
     void *fn = dtype == 0 ? geometry_kernel_for<0>(head_dim) : geometry_kernel_for<1>(head_dim);
     return launch(fn, num_seqs, lds_bytes, stream, p);
+}
+
+hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_dim, int group,
+                       size_t split_lds, hipStream_t stream) {
+    void *fs = dtype == 0 ? attn_kernel_for<0>(head_dim, group, false) : attn_kernel_for<1>(head_dim, group, false);
+    void *fc = dtype == 0 ? attn_kernel_for<0>(head_dim, group, true) : attn_kernel_for<1>(head_dim, group, true);
+    if (!fs || !fc) return hipErrorInvalidDeviceFunction;
+    void *args[] = {const_cast<UnitParams *>(&p)};
+    const unsigned sz = (unsigned)(num_seqs * p.num_layers);
+    hipError_t e = hipLaunchKernel(fs, dim3(p.splits, p.num_kv_heads, sz), dim3(kAttnThreads), args,
+                                   split_lds, stream);
+    if (e != hipSuccess) return e;
+    return hipLaunchKernel(fc, dim3(p.num_kv_heads, sz), dim3(kAttnThreads), args, 0, stream);
 }
 
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream) {

@@ -59,6 +59,15 @@ struct UnitParams {
     const uint8_t *keep_in;   // compact kernel input
     float *mean_out;          // [U][D] or null
     double *geom_out;         // [U][5] (geometry kernel)
+    // fused decode attention
+    const float *q;           // [S][L][Hq][D] of the launch's first sequence
+    float *attn_out;          // [S][L][Hq][D]
+    float *ws_acc;            // [U][splits][G][D] partial outputs (unnormalised)
+    float *ws_ml;             // [U][splits][G][2] partial max logit (log2 units) and weight sum
+    unsigned long long *ws_amin;  // [U][splits] (key << 32 | ~slot) of the lowest score
+    int32_t splits, split_rows;   // row splits per unit and rows per split
+    float qscale;             // softmax scale times log2(e)
+    int32_t pad1;
     int32_t nN[2 * kMaxSeqsPerLaunch];   // n and N of each sequence of the launch, interleaved
 };
 
@@ -69,6 +78,11 @@ hipError_t launch_select(const UnitParams &p, int num_seqs, size_t lds_bytes,
                          hipStream_t stream);
 hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                           size_t lds_bytes, hipStream_t stream);
+// Fused decode attention: split kernel (grid splits x heads x seqs*layers),
+// then the combine kernel (grid heads x seqs*layers); G = query heads per KV head.
+constexpr int kAttnThreads = 256;
+hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_dim, int group,
+                       size_t split_lds, hipStream_t stream);
 hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                            size_t lds_bytes, hipStream_t stream);
 // Reads n16 16-byte words once over the whole GPU (a measurement aid).

@@ -25,7 +25,7 @@ MAX_CAPACITY = 16384
 
 EXPORTS = ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step",
            "vd_evict_step_workspace_size", "vd_status_string", "vd_stream_read",
-           "vd_geometry")
+           "vd_geometry", "vd_decode_attention_evict", "vd_decode_attention_workspace_size")
 
 
 class VdError(RuntimeError):
@@ -74,6 +74,10 @@ def load():
     lib.vd_stream_read.restype = ctypes.c_int
     lib.vd_geometry.argtypes = [D, P, P, P]
     lib.vd_geometry.restype = ctypes.c_int
+    lib.vd_decode_attention_evict.argtypes = [D, P, ctypes.c_float, P, P, P, P, P, P, SZ, P]
+    lib.vd_decode_attention_evict.restype = ctypes.c_int
+    lib.vd_decode_attention_workspace_size.argtypes = [D]
+    lib.vd_decode_attention_workspace_size.restype = ctypes.c_size_t
     _lib = lib
     return lib
 
@@ -225,6 +229,43 @@ def vd_geometry(k, v, n_valid, out=None, *, stream=None):
     _need(out, "out", torch.float64, U * 5, v.device)
     _check("vd_geometry", load().vd_geometry(ctypes.byref(desc), _ptr(n_h), _ptr(out),
                                              _stream(v.device, stream)))
+    return out
+
+
+def vd_decode_attention_workspace_size(k, v, num_q_heads):
+    desc = cache_desc(v, k, num_q_heads)
+    return int(load().vd_decode_attention_workspace_size(ctypes.byref(desc)))
+
+
+def vd_decode_attention_evict(k, v, q, n_valid, budget, running_sum, scale=None, pos=None,
+                              out=None, workspace=None, *, stream=None):
+    """One decode step fused with its eviction (see ``vd_decode_attention_evict``
+    in vd.h): q is float32 [S, L, Hq, D]; returns the attention output (float32,
+    q's shape).  K, V, pos and the running sum are updated in place."""
+    if k is None:
+        raise ValueError("vd_decode_attention_evict needs k")
+    S, L, H, C, Dh = v.shape
+    if q.dim() != 4 or q.shape[0] != S or q.shape[1] != L or q.shape[3] != Dh:
+        raise ValueError("q must be [S, L, Hq, D] matching the cache")
+    U = _units(v)
+    desc = cache_desc(v, k, q.shape[2])
+    n_h = _host_i32(n_valid, S, "n_valid")
+    b_h = _host_i32(budget, S, "budget")
+    _need(q, "q", torch.float32, q.numel(), v.device)
+    _need(running_sum, "running_sum", torch.float64, U * (Dh + 1), v.device)
+    if pos is not None:
+        _need(pos, "pos", torch.int32, U * C, v.device)
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.float32, device=v.device)
+    _need(out, "out", torch.float32, q.numel(), v.device)
+    ws_need = int(load().vd_decode_attention_workspace_size(ctypes.byref(desc)))
+    if workspace is None:
+        workspace = torch.zeros(max(ws_need, 16), dtype=torch.uint8, device=v.device)
+    ws_bytes = workspace.numel() * workspace.element_size()
+    sc = float(Dh) ** -0.5 if scale is None else float(scale)
+    _check("vd_decode_attention_evict", load().vd_decode_attention_evict(
+        ctypes.byref(desc), _ptr(q), sc, _ptr(n_h), _ptr(b_h), _ptr(running_sum), _ptr(pos),
+        _ptr(out), _ptr(workspace), ws_bytes, _stream(v.device, stream)))
     return out
 
 
