@@ -1585,14 +1585,21 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
 // evicts (n = N + 1: the row with the lowest score, the highest slot among
 // equal lowest scores; Sec. 2.1, Eq. eviction), moves row N into the freed
 // slot below N (slot reuse) and updates the running sum.  Launched after the
-// split kernel, so every row has been read before anything moves.  The loads
-// that do not depend on the evicted slot (state, rows not in the state,
-// partials, argmin words) all go out first.
+// split kernel, so every row has been read before anything moves.
+//
+// The eviction is the work of the first LPR threads, thread c owning the
+// columns of chunk c of a row: it loads the argmin words, its state columns
+// and its chunk of the newest row (row N when evicting) all at once, and only
+// the chunk of the evicted row waits for the argmin.  Each thread reads that
+// chunk before it overwrites it, so no barrier is needed; the other threads
+// merge the outputs meanwhile.
 template <int DT, int D, int G>
 __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitParams p) {
     using A = AttnShape<DT, D>;
+    using E = Elem<DT>;
+    constexpr int EPL = A::EPL, LPR = A::LPR;
     constexpr int kOut = (G * D + kAttnThreads - 1) / kAttnThreads;  // outputs per thread
-    __shared__ int jev;
+    static_assert(LPR <= kAttnThreads, "one thread per chunk of a row");
     const int head = blockIdx.x;
     const int sl = blockIdx.y / p.num_layers, layer = blockIdx.y % p.num_layers;
     const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
@@ -1605,21 +1612,49 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     double *st = p.running_sum + u * (D + 1);
     const int S = p.splits;
     const bool evict = n > N;  // the host admits n <= N + 1 only
-    // state and the rows it does not cover
-    const int count = state_count(st + D, n);
-    double part = 0.0;
-    if (threadIdx.x < D) {
-        const int t = threadIdx.x;
-        double f = 0.0;
-        for (int r = count; r < n; ++r) f += (double)row_elem<DT>(vb + (size_t)r * ss32, t);
-        part = (count > 0 ? st[t] : 0.0) + f;
-    }
-    // the evicted slot
-    if (threadIdx.x < 64) {
+    if (threadIdx.x < LPR) {
+        const int c = threadIdx.x;
+        // everything that does not depend on the evicted slot
         unsigned long long m = ~0ull;
-        for (int s = threadIdx.x; s < S; s += 64) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
-        m = wave_min_u64(m);
-        if (threadIdx.x == 0) jev = evict ? (int)~(uint32_t)m : -1;
+        for (int s = 0; s < S; ++s) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
+        const double cnt = st[D];
+        double old[EPL];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) old[i] = st[c * EPL + i];
+        const int last = n > 0 ? n - 1 : 0;
+        const uint4 kl = load_stream(kb, row_off(last, ss32, c));
+        const uint4 vl = load_stream(vb, row_off(last, ss32, c));
+        const int32_t pl = (p.pos && evict && c == 0) ? p.pos[u * p.capacity + N] : 0;
+        const int count = (cnt >= 0.0 && cnt <= (double)n && cnt == (double)(int)cnt) ? (int)cnt : 0;
+        // the rows the state does not cover, in slot order (the newest one is loaded)
+        double f[EPL];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) f[i] = 0.0;
+        for (int r = count; r < n; ++r) {
+            float x[EPL];
+            E::unpack(r == last ? vl : load_stream(vb, row_off(r, ss32, c)), x);
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) f[i] += (double)x[i];
+        }
+        double part[EPL];
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) part[i] = (count > 0 ? old[i] : 0.0) + f[i];
+        // the evicted row leaves the running sum, read before the move below
+        const int j = evict ? (int)~(uint32_t)m : -1;
+        if (j >= 0) {
+            float x[EPL];
+            E::unpack(load_stream(vb, row_off(j, ss32, c)), x);
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) part[i] -= (double)x[i];
+        }
+#pragma unroll
+        for (int i = 0; i < EPL; ++i) st[c * EPL + i] = part[i];
+        if (c == 0) st[D] = (double)(evict ? N : n);
+        if (j >= 0 && j < N) {  // slot reuse: the newest kept row N (= n - 1) fills the hole
+            store_stream(kb, row_off(j, ss32, c), kl);
+            store_stream(vb, row_off(j, ss32, c), vl);
+            if (p.pos && c == 0) p.pos[u * p.capacity + j] = pl;
+        }
     }
     // outputs
     float *orow = p.attn_out + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
@@ -1641,23 +1676,6 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
             }
             orow[g * D + c] = n > 0 ? num / den : 0.f;
         }
-    }
-    __syncthreads();
-    const int j = jev;
-    // running sum minus the evicted row, read before the move below
-    if (threadIdx.x < D) {
-        const double ev = j >= 0 ? (double)row_elem<DT>(vb + (size_t)j * ss32, threadIdx.x) : 0.0;
-        st[threadIdx.x] = part - ev;
-    }
-    if (threadIdx.x == 0) st[D] = (double)(evict ? N : n);
-    __syncthreads();
-    if (j >= 0 && j < N) {  // slot reuse: the newest kept row N fills the hole
-        for (int c = threadIdx.x; c < 2 * A::LPR; c += kAttnThreads) {
-            char *base = c < A::LPR ? kb : vb;
-            const int ch = c % A::LPR;
-            store_stream(base, row_off(j, ss32, ch), load_stream(base, row_off(N, ss32, ch)));
-        }
-        if (p.pos && threadIdx.x == 0) p.pos[u * p.capacity + j] = p.pos[u * p.capacity + N];
     }
 }
 
