@@ -1384,12 +1384,17 @@ template <int DT> void *geometry_kernel_for(int head_dim) {
 // measured several times slower.)
 //
 // Softmax runs in log2 units (the query is pre-scaled by scale * log2(e)) with
-// a running maximum: every lane group keeps, per head, the largest logit so
-// far, the sum of 2^(z - max) and the weighted sum of its value columns,
-// rescaled when the maximum grows; two rows are taken at a time.
+// a running reference: every lane group keeps, per head, a reference logit,
+// the sum of 2^(z - reference) and the weighted sum of its value columns,
+// rescaled when the reference is raised; two rows are taken at a time.
 constexpr int kAttnWaves = kAttnThreads / 64;
 constexpr float kNoLogit = -1.0e30f;  // below every logit, finite (2^(kNoLogit - z) = 0)
 constexpr int kAttnRows = 2;           // rows per lane group in one tile of the split kernel
+// Lazy rescaling: a lane group's softmax reference (its largest logit so far,
+// in log2 units) is raised only when a logit exceeds it by more than this, so
+// every weight 2^(z - reference) stays at most 2^8 and most tiles leave the
+// running sums unscaled.  The merges take each part's reference, whatever it is.
+constexpr float kLazyLog2 = 8.0f;
 
 template <int DT, int D> struct AttnShape {
     static constexpr int EPL = Elem<DT>::EPL;
@@ -1517,27 +1522,42 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 const unsigned long long pk = ((unsigned long long)key << 32) | (uint32_t)~(uint32_t)e;
                 amin = valid[r] && pk < amin ? pk : amin;
             }
+            // the reference moves only when a logit passes it by more than
+            // kLazyLog2 (a wave-uniform branch, taken by few tiles)
+            bool grow = false;
+#pragma unroll
+            for (int g = 0; g < G; ++g)
+#pragma unroll
+                for (int r = 0; r < kAttnRows; ++r) grow = grow || z[r][g] > mx[g] + kLazyLog2;
+            if (__builtin_amdgcn_ballot_w64(grow)) {
+#pragma unroll
+                for (int g = 0; g < G; ++g) {
+                    float mn = mx[g];
+#pragma unroll
+                    for (int r = 0; r < kAttnRows; ++r) mn = fmaxf(mn, z[r][g]);
+                    const float c = __builtin_amdgcn_exp2f(mx[g] - mn);
+#pragma unroll
+                    for (int i = 0; i < EPL; ++i) acc[g][i] *= c;
+                    ls[g] *= c;
+                    mx[g] = mn;
+                }
+            }
 #pragma unroll
             for (int g = 0; g < G; ++g) {
-                float mn = mx[g];
-#pragma unroll
-                for (int r = 0; r < kAttnRows; ++r) mn = fmaxf(mn, z[r][g]);
                 float w[kAttnRows], ws = 0.f;
 #pragma unroll
                 for (int r = 0; r < kAttnRows; ++r) {
-                    w[r] = valid[r] ? __builtin_amdgcn_exp2f(z[r][g] - mn) : 0.f;
+                    w[r] = valid[r] ? __builtin_amdgcn_exp2f(z[r][g] - mx[g]) : 0.f;
                     ws += w[r];
                 }
-                const float c = __builtin_amdgcn_exp2f(mx[g] - mn);
 #pragma unroll
                 for (int i = 0; i < EPL; ++i) {
-                    float x = acc[g][i] * c;
+                    float x = acc[g][i];
 #pragma unroll
                     for (int r = 0; r < kAttnRows; ++r) x = fmaf(w[r], vx[r][i], x);
                     acc[g][i] = x;
                 }
-                ls[g] = fmaf(ls[g], c, ws);
-                mx[g] = mn;
+                ls[g] += ws;
             }
         }
     }
