@@ -66,8 +66,14 @@ def kept_from_pos(post_pos, n, N):
 
 
 def run_case(orc, S, L, H, G, C, D, dtype, n, N, seed, qscale=1.0, same_rows=False,
-             sample=None, count=None):
+             sample=None, count=None, k_ramp=None):
     k, v = make_cache(S, L, H, C, D, dtype, n, seed, same_rows)
+    if k_ramp is not None:
+        # every key row is slot 0's row times (1 + k_ramp * slot)
+        j = torch.arange(C, device=DEV, dtype=torch.float32).view(1, 1, 1, C, 1)
+        k.copy_((k[:, :, :, :1].float() * (1.0 + k_ramp * j)).to(dtype))
+        for s in range(S):
+            k[s, :, :, n[s]:] = float("nan")
     U = S * L * H
     n_u, N_u = per_unit(n, L, H), per_unit(N, L, H)
     cnt = np.maximum(n_u - 1, 0) if count is None else per_unit(count, L, H)
@@ -133,6 +139,17 @@ def test_decode_step_sharp_softmax(orc):
     # large queries: the softmax is nearly one-hot
     rep, *_ = run_case(orc, 2, 1, 2, 4, 520, 128, torch.bfloat16, [513, 400], [512, 399],
                        seed=63, qscale=30.0)
+    print(rep)
+
+
+def test_decode_step_rising_logits(orc):
+    # keys along one direction with a growing length: for the query heads that
+    # face it the logits rise along the slots, so each lane group raises its
+    # softmax reference again and again, by steps above and below 2^8; 128
+    # units give 6 splits of 6 tiles per lane group
+    S, H = 16, 8
+    rep, *_ = run_case(orc, S, 1, H, 4, 1040, 128, torch.bfloat16, [1025] * S, [1024] * S,
+                       seed=67, qscale=2.0, k_ramp=0.05)
     print(rep)
 
 
