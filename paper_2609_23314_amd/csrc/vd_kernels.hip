@@ -1395,6 +1395,7 @@ constexpr int kAttnRows = 2;           // rows per lane group in one tile of the
 // every weight 2^(z - reference) stays at most 2^8 and most tiles leave the
 // running sums unscaled.  The merges take each part's reference, whatever it is.
 constexpr float kLazyLog2 = 8.0f;
+constexpr int kMergeBatch = 8;  // splits whose partials the combine loads at once
 
 template <int DT, int D> struct AttnShape {
     static constexpr int EPL = Elem<DT>::EPL;
@@ -1685,14 +1686,35 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
         const int idx = threadIdx.x + o * kAttnThreads;
         if (idx < G * D) {
             const int g = idx / D, c = idx % D;
+            // splits in batches of kMergeBatch whose loads all go out together
+            // (a split past S reads split s0 again and weighs 0)
             float top = kNoLogit;
-            for (int s = 0; s < S; ++s) top = fmaxf(top, ml[(s * G + g) * 2]);
+            for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
+                float m[kMergeBatch];
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) {
+                    const int s = s0 + i < S ? s0 + i : s0;
+                    m[i] = ml[(s * G + g) * 2];
+                }
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) top = fmaxf(top, m[i]);
+            }
             float num = 0.f, den = 0.f;
-#pragma unroll 4
-            for (int s = 0; s < S; ++s) {
-                const float f = __builtin_amdgcn_exp2f(ml[(s * G + g) * 2] - top);
-                num = fmaf(pa[(s * G + g) * D + c], f, num);
-                den = fmaf(ml[(s * G + g) * 2 + 1], f, den);
+            for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
+                float m[kMergeBatch], l[kMergeBatch], a[kMergeBatch];
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) {
+                    const int s = s0 + i < S ? s0 + i : s0;
+                    m[i] = ml[(s * G + g) * 2];
+                    l[i] = ml[(s * G + g) * 2 + 1];
+                    a[i] = pa[(s * G + g) * D + c];
+                }
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) {
+                    const float f = s0 + i < S ? __builtin_amdgcn_exp2f(m[i] - top) : 0.f;
+                    num = fmaf(a[i], f, num);
+                    den = fmaf(l[i], f, den);
+                }
             }
             orow[g * D + c] = n > 0 ? num / den : 0.f;
         }
