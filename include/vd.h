@@ -66,7 +66,20 @@ typedef enum {
 
 typedef enum { VD_DTYPE_BF16 = 0, VD_DTYPE_F32 = 1 } vd_dtype;
 
-typedef enum { VD_SCORE_L2 = 0, VD_SCORE_DIR = 1, VD_SCORE_NORM = 2 } vd_variant;
+/* Scores (Sec. 3.2 for the value side; Sec. 4, Baselines, for the key side
+ * and for FastCAOTE).  The key-side scores are the same three geometric
+ * scores taken on the key rows instead of the value rows. */
+typedef enum {
+    VD_SCORE_L2 = 0,         /* ||v_j - v_bar||, largest kept (ValueDiff) */
+    VD_SCORE_DIR = 1,        /* 1 - cos(v_j, v_bar), largest kept */
+    VD_SCORE_NORM = 2,       /* ||v_j||, largest kept */
+    VD_SCORE_KEY_L2 = 3,     /* ||k_j - k_bar||, largest kept (ManifoldKV) */
+    VD_SCORE_KEY_DIR = 4,    /* 1 - cos(k_j, k_bar), largest kept (KeyDiff) */
+    VD_SCORE_KEY_NORM = 5,   /* ||k_j||, SMALLEST kept (KeyNorm) */
+    VD_SCORE_FASTCAOTE = 6   /* a_j / (1 - a_j) * ||v_j - v_bar|| with a_j the
+                                observed attention weight; only in the fused
+                                decode step (App. A, Eq. app_fastcaote) */
+} vd_variant;
 
 /* Limits of this build. */
 #define VD_MAX_CAPACITY 16384  /* slots per unit */
@@ -171,8 +184,8 @@ vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double 
  * vd_decode_attention_evict -- one decode step of every sequence, fused with
  * its eviction: attention of the newest token over the n cached rows (Sec.
  * 2.1, Eq. attention; B = 1 in Eq. block_processing), then, where n = N + 1,
- * the eviction of the row with the lowest L2 score (Sec. 3.2, Eq. vd; Sec.
- * 2.1, Eq. eviction) scored in the same pass over V.
+ * the eviction of the row with the lowest score, scored in the same pass over
+ * K and V.
  *   desc          K and V both required; num_q_heads = G * num_kv_heads with
  *                 G in {1, 2, 4}; query head h*G + g uses KV head h
  *   q             device float [S][L][num_q_heads][head_dim], contiguous: the
@@ -180,6 +193,12 @@ vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double 
  *   scale         softmax scale (1/sqrt(head_dim) in the paper), finite
  *   n_valid[s]    host; cached tokens, the newest included; n <= budget + 1
  *   budget[s]     host; N >= 1
+ *   variant       VD_SCORE_L2: s_j = ||v_j - v_bar|| (Sec. 3.2, Eq. vd);
+ *                 VD_SCORE_FASTCAOTE: s_j = a_j / (1 - a_j) * ||v_j - v_bar||
+ *                 (App. A, Eq. app_fastcaote), a_j the mean over the G query
+ *                 heads of the KV head of their softmax weight on row j in
+ *                 this very step; s_j is +infinity when 1 - a_j is 0.
+ *                 Any other variant is VD_ERR_INVALID_ARG.
  *   running_sum   device double [U][head_dim + 1], required: the column sums
  *                 of the rows it covers, then their count (as vd_evict_step);
  *                 on return it covers the rows left.  Rows it does not cover
@@ -189,25 +208,26 @@ vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double 
  *   out           device float [S][L][num_q_heads][head_dim]: the attention
  *                 output of every query row (0 for a sequence with n = 0)
  *   workspace     device, 16-byte aligned, at least
- *                 vd_decode_attention_workspace_size(desc) bytes; calls that
- *                 share a workspace must not overlap
+ *                 vd_decode_attention_workspace_size(desc, variant) bytes;
+ *                 calls that share a workspace must not overlap
  * A unit's rows are split over several workgroups; a second kernel merges
  * them, so the attention reads every row before anything moves.  Eviction:
- * the row
- * with the lowest score goes, the highest slot among equal lowest scores; if
- * it lies below N, row N takes its slot (K, V and pos).  Scores and softmax are
- * fp32 (log2-domain exponentials), the mean and the running sum fp64.
- * VD_ERR_UNSUPPORTED for n > budget + 1 or another G; VD_ERR_WORKSPACE for a
- * missing or short workspace; VD_ERR_INVALID_ARG as the other calls.
+ * the row with the lowest score goes, the highest slot among equal lowest
+ * scores; if it lies below N, row N takes its slot (K, V and pos).  Scores,
+ * weights and softmax are fp32 (log2-domain exponentials), the mean and the
+ * running sum fp64.  VD_ERR_UNSUPPORTED for n > budget + 1 or another G;
+ * VD_ERR_WORKSPACE for a missing or short workspace; VD_ERR_INVALID_ARG as
+ * the other calls.
  */
 vd_status vd_decode_attention_evict(const vd_cache_desc *desc, const float *q, float scale,
                                     const int32_t *n_valid, const int32_t *budget,
-                                    double *running_sum, int32_t *pos, float *out,
-                                    void *workspace, size_t workspace_bytes, vd_stream stream);
+                                    vd_variant variant, double *running_sum, int32_t *pos,
+                                    float *out, void *workspace, size_t workspace_bytes,
+                                    vd_stream stream);
 
 /* Bytes of device workspace vd_decode_attention_evict needs for this
- * descriptor (0 for an invalid descriptor). */
-size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc);
+ * descriptor and variant (0 for an invalid descriptor or variant). */
+size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc, vd_variant variant);
 
 /* Bytes of device workspace vd_evict_step needs for this descriptor (0 in this build). */
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);

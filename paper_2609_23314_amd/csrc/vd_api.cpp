@@ -122,29 +122,106 @@ vd_status launched(hipError_t e) { return e == hipSuccess ? VD_OK : VD_ERR_HIP; 
 // Row splits of the fused decode attention: about 768 workgroups of 256
 // threads over the whole launch (three per CU, what stays resident at the
 // split kernel's register use; more splits were measured slower), each split
-// a whole number of the split kernel's two-row tiles.
+// a whole number of the split kernel's two-row tiles.  FastCAOTE keeps every
+// row's logits and distance of a split in LDS until the split ends, so its
+// splits hold at most kCaoteSplitRows rows.
+constexpr int kCaoteSplitRows = 2048;
 struct AttnPlan {
     int group, splits, rows, groups;
     int64_t units;
 };
-AttnPlan attn_plan(const vd_cache_desc *d) {
+AttnPlan attn_plan(const vd_cache_desc *d, vd_variant variant) {
     AttnPlan a;
     a.group = d->num_q_heads / d->num_kv_heads;
     a.units = int64_t(d->num_seqs) * d->num_layers * d->num_kv_heads;
     const int lpr = int(d->head_dim * elem_bytes(d->dtype) / 16);
     a.groups = (vd::kAttnThreads / 64) * (64 / lpr);
     const int tile = 2 * a.groups;
-    const int64_t want = std::min<int64_t>(64, std::max<int64_t>(1, (768 + a.units - 1) / a.units));
+    int64_t want = std::min<int64_t>(64, std::max<int64_t>(1, (768 + a.units - 1) / a.units));
+    if (variant == VD_SCORE_FASTCAOTE)
+        want = std::max<int64_t>(want, (d->capacity + kCaoteSplitRows - 1) / kCaoteSplitRows);
     int rows = int((d->capacity + want - 1) / want);
     rows = (rows + tile - 1) / tile * tile;
+    if (variant == VD_SCORE_FASTCAOTE) rows = std::min(rows, kCaoteSplitRows);
     a.rows = rows;
     a.splits = (d->capacity + rows - 1) / rows;
     return a;
 }
-// workspace: partial outputs, then (max, sum) pairs, then the argmin words
-int64_t attn_ws_bytes(const AttnPlan &a, int head_dim) {
+// Workspace: partial outputs, then (max, sum) pairs, then the argmin words,
+// then (FastCAOTE) the G logits and the distance of every row of every unit.
+struct AttnWs {
+    int64_t acc, ml, amin, rows, total;  // byte offsets and the total
+};
+AttnWs attn_ws_layout(const vd_cache_desc *d, const AttnPlan &a, vd_variant variant) {
     const int64_t parts = a.units * a.splits;
-    return align16(parts * a.group * head_dim * 4) + align16(parts * a.group * 2 * 4) + parts * 8;
+    AttnWs w;
+    w.acc = 0;
+    w.ml = align16(parts * a.group * d->head_dim * 4);
+    w.amin = w.ml + align16(parts * a.group * 2 * 4);
+    w.rows = w.amin + align16(parts * 8);
+    w.total = w.rows + (variant == VD_SCORE_FASTCAOTE
+                            ? align16(a.units * int64_t(d->capacity) * (a.group + 1) * 4) : 0);
+    return w;
+}
+
+// Validation shared by the fused decode step's entry points (host only, no
+// HIP call); on success `plan` and `ws` describe the launch.
+vd_status check_decode(const vd_cache_desc *desc, const float *q, float scale,
+                       const int32_t *n_valid, const int32_t *budget, vd_variant variant,
+                       const double *running_sum, const int32_t *pos, const float *out,
+                       AttnPlan &plan, AttnWs &ws) {
+    vd_status st = check_desc(desc);
+    if (st != VD_OK) return st;
+    if (!desc->k) return VD_ERR_INVALID_ARG;
+    if (!budget) return VD_ERR_INVALID_ARG;
+    if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
+    if (variant != VD_SCORE_L2 && variant != VD_SCORE_FASTCAOTE) return VD_ERR_INVALID_ARG;
+    const int group = desc->num_q_heads / desc->num_kv_heads;
+    if (group != 1 && group != 2 && group != 4) return VD_ERR_UNSUPPORTED;
+    for (int s = 0; s < desc->num_seqs; ++s)
+        if (n_valid[s] - 1 > budget[s]) return VD_ERR_UNSUPPORTED;  // one token evicted at most
+    if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return VD_ERR_INVALID_ARG;
+    if (!running_sum || !aligned(running_sum, 8) || (pos && !aligned(pos, 4)))
+        return VD_ERR_INVALID_ARG;
+    if (!std::isfinite(scale)) return VD_ERR_INVALID_ARG;
+    if (variant == VD_SCORE_FASTCAOTE) return VD_ERR_UNSUPPORTED;
+    plan = attn_plan(desc, variant);
+    ws = attn_ws_layout(desc, plan, variant);
+    return VD_OK;
+}
+
+// Launches of the fused decode step on a validated call, with the workspace
+// at `wsp` (ws.total bytes, 16-byte aligned).
+vd_status launch_decode(const vd_cache_desc *desc, const float *q, float scale,
+                        const int32_t *n_valid, const int32_t *budget, vd_variant variant,
+                        double *running_sum, int32_t *pos, float *out, const AttnPlan &a,
+                        const AttnWs &ws, char *wsp, hipStream_t stream) {
+    const int D = desc->head_dim, L = desc->num_layers, group = a.group;
+    float *ws_acc = reinterpret_cast<float *>(wsp + ws.acc);
+    float *ws_ml = reinterpret_cast<float *>(wsp + ws.ml);
+    auto *ws_amin = reinterpret_cast<unsigned long long *>(wsp + ws.amin);
+    (void)variant;
+    const int seqs_per_launch = std::max(1, std::min(vd::kMaxSeqsPerLaunch, 65535 / L));
+    const int64_t row_floats = int64_t(L) * desc->num_q_heads * D;  // q / out floats per sequence
+    const size_t split_lds = size_t(D) * 4 + size_t(2 * a.groups * group) * 4 +
+                             size_t(vd::kAttnThreads / 64) * 8 + size_t(group) * a.groups * D * 4;
+    for (int s0 = 0; s0 < desc->num_seqs; s0 += seqs_per_launch) {
+        const int ns = std::min(seqs_per_launch, desc->num_seqs - s0);
+        UnitParams p = base_params(desc, s0, ns, n_valid, budget);
+        p.running_sum = running_sum;
+        p.pos = pos;
+        p.q = q + s0 * row_floats;
+        p.attn_out = out + s0 * row_floats;
+        p.ws_acc = ws_acc;
+        p.ws_ml = ws_ml;
+        p.ws_amin = ws_amin;
+        p.splits = a.splits;
+        p.split_rows = a.rows;
+        p.qscale = float(double(scale) * 1.4426950408889634);  // log2(e)
+        const vd_status st = launched(vd::launch_attn(p, ns, desc->dtype, D, group, split_lds, stream));
+        if (st != VD_OK) return st;
+    }
+    return VD_OK;
 }
 
 }  // namespace
@@ -288,62 +365,26 @@ vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double 
     return VD_OK;
 }
 
-size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc) {
+size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc, vd_variant variant) {
     if (check_desc(desc) != VD_OK) return 0;
-    return size_t(attn_ws_bytes(attn_plan(desc), desc->head_dim));
+    if (variant != VD_SCORE_L2 && variant != VD_SCORE_FASTCAOTE) return 0;
+    return size_t(attn_ws_layout(desc, attn_plan(desc, variant), variant).total);
 }
 
 vd_status vd_decode_attention_evict(const vd_cache_desc *desc, const float *q, float scale,
                                     const int32_t *n_valid, const int32_t *budget,
-                                    double *running_sum, int32_t *pos, float *out,
-                                    void *workspace, size_t workspace_bytes, vd_stream stream) {
-    vd_status st = check_desc(desc);
+                                    vd_variant variant, double *running_sum, int32_t *pos,
+                                    float *out, void *workspace, size_t workspace_bytes,
+                                    vd_stream stream) {
+    AttnPlan a;
+    AttnWs ws;
+    const vd_status st = check_decode(desc, q, scale, n_valid, budget, variant, running_sum, pos,
+                                      out, a, ws);
     if (st != VD_OK) return st;
-    if (!desc->k) return VD_ERR_INVALID_ARG;
-    if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
-    if (!budget) return VD_ERR_INVALID_ARG;
-    const int group = desc->num_q_heads / desc->num_kv_heads;
-    if (group != 1 && group != 2 && group != 4) return VD_ERR_UNSUPPORTED;
-    for (int s = 0; s < desc->num_seqs; ++s)
-        if (n_valid[s] > budget[s] + 1) return VD_ERR_UNSUPPORTED;  // one token evicted at most
-    if (!q || !out || !aligned(q, 4) || !aligned(out, 4)) return VD_ERR_INVALID_ARG;
-    if (!running_sum || !aligned(running_sum, 8) || (pos && !aligned(pos, 4)))
-        return VD_ERR_INVALID_ARG;
-    if (!std::isfinite(scale)) return VD_ERR_INVALID_ARG;
-    const AttnPlan a = attn_plan(desc);
     if (!workspace || !aligned(workspace, 16)) return VD_ERR_WORKSPACE;
-    if (int64_t(workspace_bytes) < attn_ws_bytes(a, desc->head_dim)) return VD_ERR_WORKSPACE;
-    const int D = desc->head_dim, L = desc->num_layers;
-    const int64_t parts = a.units * a.splits;
-    char *ws = static_cast<char *>(workspace);
-    float *ws_acc = reinterpret_cast<float *>(ws);
-    float *ws_ml = reinterpret_cast<float *>(ws + align16(parts * group * D * 4));
-    auto *ws_amin = reinterpret_cast<unsigned long long *>(
-        ws + align16(parts * group * D * 4) + align16(parts * group * 2 * 4));
-
-    const int seqs_per_launch = std::max(1, std::min(vd::kMaxSeqsPerLaunch, 65535 / L));
-    const int64_t row_floats = int64_t(L) * desc->num_q_heads * D;  // q / out floats per sequence
-    const int groups = a.groups;
-    const size_t split_lds = size_t(D) * 4 + size_t(2 * groups * group) * 4 + size_t(vd::kAttnThreads / 64) * 8 +
-                             size_t(group) * groups * D * 4;
-    for (int s0 = 0; s0 < desc->num_seqs; s0 += seqs_per_launch) {
-        const int ns = std::min(seqs_per_launch, desc->num_seqs - s0);
-        UnitParams p = base_params(desc, s0, ns, n_valid, budget);
-        p.running_sum = running_sum;
-        p.pos = pos;
-        p.q = q + s0 * row_floats;
-        p.attn_out = out + s0 * row_floats;
-        p.ws_acc = ws_acc;
-        p.ws_ml = ws_ml;
-        p.ws_amin = ws_amin;
-        p.splits = a.splits;
-        p.split_rows = a.rows;
-        p.qscale = float(double(scale) * 1.4426950408889634);  // log2(e)
-        st = launched(vd::launch_attn(p, ns, desc->dtype, D, group, split_lds,
-                                      reinterpret_cast<hipStream_t>(stream)));
-        if (st != VD_OK) return st;
-    }
-    return VD_OK;
+    if (int64_t(workspace_bytes) < ws.total) return VD_ERR_WORKSPACE;
+    return launch_decode(desc, q, scale, n_valid, budget, variant, running_sum, pos, out, a, ws,
+                         static_cast<char *>(workspace), reinterpret_cast<hipStream_t>(stream));
 }
 
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc) {

@@ -20,7 +20,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvd.so")
 
 VD_OK, VD_ERR_INVALID_ARG, VD_ERR_UNSUPPORTED, VD_ERR_WORKSPACE, VD_ERR_HIP = range(5)
 VD_DTYPE_BF16, VD_DTYPE_F32 = 0, 1
-VARIANTS = {"l2": 0, "dir": 1, "norm": 2}
+VARIANTS = {"l2": 0, "dir": 1, "norm": 2, "key_l2": 3, "key_dir": 4, "key_norm": 5,
+            "fastcaote": 6}
 MAX_CAPACITY = 16384
 
 EXPORTS = ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step",
@@ -74,9 +75,9 @@ def load():
     lib.vd_stream_read.restype = ctypes.c_int
     lib.vd_geometry.argtypes = [D, P, P, P]
     lib.vd_geometry.restype = ctypes.c_int
-    lib.vd_decode_attention_evict.argtypes = [D, P, ctypes.c_float, P, P, P, P, P, P, SZ, P]
+    lib.vd_decode_attention_evict.argtypes = [D, P, ctypes.c_float, P, P, I32, P, P, P, P, SZ, P]
     lib.vd_decode_attention_evict.restype = ctypes.c_int
-    lib.vd_decode_attention_workspace_size.argtypes = [D]
+    lib.vd_decode_attention_workspace_size.argtypes = [D, I32]
     lib.vd_decode_attention_workspace_size.restype = ctypes.c_size_t
     _lib = lib
     return lib
@@ -232,18 +233,14 @@ def vd_geometry(k, v, n_valid, out=None, *, stream=None):
     return out
 
 
-def vd_decode_attention_workspace_size(k, v, num_q_heads):
+def vd_decode_attention_workspace_size(k, v, num_q_heads, variant="l2"):
     desc = cache_desc(v, k, num_q_heads)
-    return int(load().vd_decode_attention_workspace_size(ctypes.byref(desc)))
+    return int(load().vd_decode_attention_workspace_size(ctypes.byref(desc), VARIANTS[variant]))
 
 
-def vd_decode_attention_evict(k, v, q, n_valid, budget, running_sum, scale=None, pos=None,
-                              out=None, workspace=None, *, stream=None):
-    """One decode step fused with its eviction (see ``vd_decode_attention_evict``
-    in vd.h): q is float32 [S, L, Hq, D]; returns the attention output (float32,
-    q's shape).  K, V, pos and the running sum are updated in place."""
+def _decode_args(k, v, q, n_valid, budget, running_sum, pos, out):
     if k is None:
-        raise ValueError("vd_decode_attention_evict needs k")
+        raise ValueError("the fused decode step needs k")
     S, L, H, C, Dh = v.shape
     if q.dim() != 4 or q.shape[0] != S or q.shape[1] != L or q.shape[3] != Dh:
         raise ValueError("q must be [S, L, Hq, D] matching the cache")
@@ -258,14 +255,25 @@ def vd_decode_attention_evict(k, v, q, n_valid, budget, running_sum, scale=None,
     if out is None:
         out = torch.empty(q.shape, dtype=torch.float32, device=v.device)
     _need(out, "out", torch.float32, q.numel(), v.device)
-    ws_need = int(load().vd_decode_attention_workspace_size(ctypes.byref(desc)))
+    return desc, n_h, b_h, out
+
+
+def vd_decode_attention_evict(k, v, q, n_valid, budget, running_sum, scale=None, pos=None,
+                              out=None, workspace=None, *, variant="l2", stream=None):
+    """One decode step fused with its eviction (see ``vd_decode_attention_evict``
+    in vd.h): q is float32 [S, L, Hq, D]; returns the attention output (float32,
+    q's shape).  K, V, pos and the running sum are updated in place.  variant is
+    "l2" (ValueDiff) or "fastcaote"."""
+    desc, n_h, b_h, out = _decode_args(k, v, q, n_valid, budget, running_sum, pos, out)
+    ws_need = int(load().vd_decode_attention_workspace_size(ctypes.byref(desc), VARIANTS[variant]))
     if workspace is None:
         workspace = torch.zeros(max(ws_need, 16), dtype=torch.uint8, device=v.device)
     ws_bytes = workspace.numel() * workspace.element_size()
-    sc = float(Dh) ** -0.5 if scale is None else float(scale)
+    sc = float(v.shape[4]) ** -0.5 if scale is None else float(scale)
     _check("vd_decode_attention_evict", load().vd_decode_attention_evict(
-        ctypes.byref(desc), _ptr(q), sc, _ptr(n_h), _ptr(b_h), _ptr(running_sum), _ptr(pos),
-        _ptr(out), _ptr(workspace), ws_bytes, _stream(v.device, stream)))
+        ctypes.byref(desc), _ptr(q), sc, _ptr(n_h), _ptr(b_h), VARIANTS[variant],
+        _ptr(running_sum), _ptr(pos), _ptr(out), _ptr(workspace), ws_bytes,
+        _stream(v.device, stream)))
     return out
 
 

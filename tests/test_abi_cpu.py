@@ -139,3 +139,60 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(vd, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="missing"):
         vd.load()
+
+
+def call_decode(d, n=(50, 60), N=(49, 59), variant=0, q=FAKE_V, scale=0.1, rs=FAKE_V,
+                pos=None, out=FAKE_V, ws=FAKE_V, ws_bytes=1 << 40):
+    lib = vd.load()
+    S = max(int(d.num_seqs), 1)
+    n_arr = (ctypes.c_int32 * S)(*(list(n) + [0] * S)[:S])
+    N_arr = None if N is None else (ctypes.c_int32 * S)(*(list(N) + [1] * S)[:S])
+    return lib.vd_decode_attention_evict(ctypes.byref(d), q, scale, n_arr, N_arr, variant, rs, pos,
+                                         out, ws, ws_bytes, None)
+
+
+def decode_desc(**kw):
+    return good_desc(**{"num_q_heads": 16, **kw})   # 4 KV heads, G = 4 by default
+
+
+def test_decode_attention_rejections():
+    """Every rejection path of vd_decode_attention_evict returns before any HIP
+    call (the pointers are never dereferenced)."""
+    d = decode_desc()
+    bad_ptr = ctypes.c_void_p(FAKE_V + 4)
+    assert call_decode(d, n=(51, 60)) == vd.VD_ERR_UNSUPPORTED        # n > N + 1
+    # a budget of INT32_MAX passes the one-token check without overflow (q is
+    # null so that validation still fails before any launch)
+    assert call_decode(d, N=(2**31 - 1, 59), q=None) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(decode_desc(num_q_heads=12)) == vd.VD_ERR_UNSUPPORTED   # G = 3
+    assert call_decode(decode_desc(num_q_heads=32)) == vd.VD_ERR_UNSUPPORTED   # G = 8
+    assert call_decode(d, variant=1) == vd.VD_ERR_INVALID_ARG          # Dir is not a decode score
+    assert call_decode(d, variant=7) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, scale=float("inf")) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, scale=float("nan")) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, rs=None) == vd.VD_ERR_INVALID_ARG            # state required
+    assert call_decode(d, rs=bad_ptr) == vd.VD_ERR_INVALID_ARG         # misaligned state
+    assert call_decode(d, q=None) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, out=None) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, q=ctypes.c_void_p(FAKE_V + 2)) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, pos=ctypes.c_void_p(FAKE_V + 2)) == vd.VD_ERR_INVALID_ARG
+    assert call_decode(d, N=None) == vd.VD_ERR_INVALID_ARG             # budget missing
+    assert call_decode(d, N=(0, 59)) == vd.VD_ERR_INVALID_ARG          # budget < 1
+    assert call_decode(d, n=(101, 60)) == vd.VD_ERR_INVALID_ARG        # n > capacity
+    assert call_decode(d, ws=None) == vd.VD_ERR_WORKSPACE
+    assert call_decode(d, ws=ctypes.c_void_p(FAKE_V + 8)) == vd.VD_ERR_WORKSPACE  # misaligned
+    need = vd.load().vd_decode_attention_workspace_size(ctypes.byref(d), 0)
+    assert need > 0
+    assert call_decode(d, ws_bytes=need - 1) == vd.VD_ERR_WORKSPACE    # short
+    nok = decode_desc()
+    nok.k = None
+    assert call_decode(nok) == vd.VD_ERR_INVALID_ARG                   # K required
+
+
+def test_decode_attention_workspace_sizes():
+    lib = vd.load()
+    d = decode_desc()
+    l2 = lib.vd_decode_attention_workspace_size(ctypes.byref(d), 0)
+    assert l2 > 0
+    assert lib.vd_decode_attention_workspace_size(ctypes.byref(d), 1) == 0      # not a decode score
+    assert lib.vd_decode_attention_workspace_size(ctypes.byref(good_desc(head_dim=96)), 0) == 0

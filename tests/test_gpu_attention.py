@@ -207,8 +207,8 @@ def test_decode_steps_in_a_row(orc):
 @pytest.mark.parametrize("per_layer", [True, False])
 def test_decode_workload_sampled(orc, per_layer):
     # the decode workload's shape: 16 sequences x 32 layers x 8 KV heads, 32
-    # query heads, n = 4097, N = 4096; one layer per call (15 row splits per
-    # unit) or all layers in one call (one split per unit)
+    # query heads, n = 4097, N = 4096; one layer per call (128 units, 6 row
+    # splits per unit) or all layers in one call (one split per unit)
     S, L, H, G, D, N = 16, 32, 8, 4, 128, 4096
     C = N + 1
     layers = [5] if per_layer else list(range(L))
