@@ -229,6 +229,32 @@ vd_status vd_decode_attention_evict(const vd_cache_desc *desc, const float *q, f
  * descriptor and variant (0 for an invalid descriptor or variant). */
 size_t vd_decode_attention_workspace_size(const vd_cache_desc *desc, vd_variant variant);
 
+/*
+ * vd_decode_attention_evict_noalloc -- vd_decode_attention_evict without a
+ * workspace argument, for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid it).
+ * The library allocates nothing here either: the split partials live in a
+ * static device array of vd_decode_attention_noalloc_max_bytes() bytes
+ * (32 MiB), one copy per GPU, held until the process ends.  Arguments,
+ * results and errors are those of vd_decode_attention_evict, and the two
+ * give bit-identical results; in addition
+ *   - VD_ERR_WORKSPACE when vd_decode_attention_workspace_size(desc, variant)
+ *     exceeds that maximum (nothing is queued);
+ *   - VD_ERR_HIP when the stream belongs to a device other than the current
+ *     one, or the array's address cannot be obtained.
+ * Every call on one GPU uses the same array and leaves its contents behind:
+ * calls that overlap on one GPU (other streams, other host threads) race
+ * and must be ordered by the caller.  Nothing needs to start at zero: each
+ * call writes every partial it reads.
+ */
+vd_status vd_decode_attention_evict_noalloc(const vd_cache_desc *desc, const float *q, float scale,
+                                            const int32_t *n_valid, const int32_t *budget,
+                                            vd_variant variant, double *running_sum, int32_t *pos,
+                                            float *out, vd_stream stream);
+
+/* Bytes of the static device array behind vd_decode_attention_evict_noalloc. */
+size_t vd_decode_attention_noalloc_max_bytes(void);
+
 /* Bytes of device workspace vd_evict_step needs for this descriptor (0 in this build). */
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc);
 

@@ -387,6 +387,25 @@ vd_status vd_decode_attention_evict(const vd_cache_desc *desc, const float *q, f
                          static_cast<char *>(workspace), reinterpret_cast<hipStream_t>(stream));
 }
 
+vd_status vd_decode_attention_evict_noalloc(const vd_cache_desc *desc, const float *q, float scale,
+                                            const int32_t *n_valid, const int32_t *budget,
+                                            vd_variant variant, double *running_sum, int32_t *pos,
+                                            float *out, vd_stream stream) {
+    AttnPlan a;
+    AttnWs ws;
+    const vd_status st = check_decode(desc, q, scale, n_valid, budget, variant, running_sum, pos,
+                                      out, a, ws);
+    if (st != VD_OK) return st;
+    if (ws.total > int64_t(vd::kScratchBytes)) return VD_ERR_WORKSPACE;  // beyond the static scratch
+    void *scratch = nullptr;
+    const hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    if (vd::scratch_memory(hs, &scratch) != hipSuccess) return VD_ERR_HIP;
+    return launch_decode(desc, q, scale, n_valid, budget, variant, running_sum, pos, out, a, ws,
+                         static_cast<char *>(scratch), hs);
+}
+
+size_t vd_decode_attention_noalloc_max_bytes(void) { return vd::kScratchBytes; }
+
 size_t vd_evict_step_workspace_size(const vd_cache_desc *desc) {
     (void)desc;
     return 0;

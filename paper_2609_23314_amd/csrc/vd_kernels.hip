@@ -32,9 +32,18 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
 #include <type_traits>
 
 #include "vd_launch.h"
+
+// Device memory of the allocation-free fused decode step: its split partials
+// live here instead of in a workspace of the caller's.  Every GPU the library
+// runs on holds its own copy until the process ends, and every call on that
+// GPU uses it (calls that overlap on one GPU race).  Host code never passes
+// this name to a kernel: it takes the address hipGetSymbolAddress gives for
+// the current device (vd::scratch_memory below).
+static __device__ __align__(256) unsigned char scratch[vd::kScratchBytes];
 
 namespace vd {
 namespace {
@@ -1839,6 +1848,31 @@ hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_di
                                    split_lds, stream);
     if (e != hipSuccess) return e;
     return hipLaunchKernel(fc, dim3(p.num_kv_heads, sz), dim3(kAttnThreads), args, 0, stream);
+}
+
+hipError_t scratch_memory(hipStream_t stream, void **ptr) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (stream) {  // the launch goes to the stream's device: it must be the current one
+        hipDevice_t sdev = -1;
+        e = hipStreamGetDevice(stream, &sdev);
+        if (e != hipSuccess) return e;
+        if (sdev != dev) return hipErrorInvalidDevice;
+    }
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {  // once per device, with that device current
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
 }
 
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream) {

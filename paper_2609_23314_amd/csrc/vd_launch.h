@@ -85,6 +85,12 @@ hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_di
                        size_t split_lds, hipStream_t stream);
 hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                            size_t lds_bytes, hipStream_t stream);
+// Static device scratch of the allocation-free fused decode step (one copy per
+// GPU): its size, and its address on the current device, which must be the
+// device of `stream` (looked up once per device, then cached).
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kMaxDevices = 64;
+hipError_t scratch_memory(hipStream_t stream, void **ptr);
 // Reads n16 16-byte words once over the whole GPU (a measurement aid).
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream);
 

@@ -26,7 +26,8 @@ MAX_CAPACITY = 16384
 
 EXPORTS = ("vd_score", "vd_select_topn", "vd_compact", "vd_evict_step",
            "vd_evict_step_workspace_size", "vd_status_string", "vd_stream_read",
-           "vd_geometry", "vd_decode_attention_evict", "vd_decode_attention_workspace_size")
+           "vd_geometry", "vd_decode_attention_evict", "vd_decode_attention_workspace_size",
+           "vd_decode_attention_evict_noalloc", "vd_decode_attention_noalloc_max_bytes")
 
 
 class VdError(RuntimeError):
@@ -78,6 +79,10 @@ def load():
     lib.vd_decode_attention_evict.argtypes = [D, P, ctypes.c_float, P, P, I32, P, P, P, P, SZ, P]
     lib.vd_decode_attention_evict.restype = ctypes.c_int
     lib.vd_decode_attention_workspace_size.argtypes = [D, I32]
+    lib.vd_decode_attention_evict_noalloc.argtypes = [D, P, ctypes.c_float, P, P, I32, P, P, P, P]
+    lib.vd_decode_attention_evict_noalloc.restype = ctypes.c_int
+    lib.vd_decode_attention_noalloc_max_bytes.argtypes = []
+    lib.vd_decode_attention_noalloc_max_bytes.restype = ctypes.c_size_t
     lib.vd_decode_attention_workspace_size.restype = ctypes.c_size_t
     _lib = lib
     return lib
@@ -275,6 +280,26 @@ def vd_decode_attention_evict(k, v, q, n_valid, budget, running_sum, scale=None,
         _ptr(running_sum), _ptr(pos), _ptr(out), _ptr(workspace), ws_bytes,
         _stream(v.device, stream)))
     return out
+
+
+def vd_decode_attention_evict_noalloc(k, v, q, n_valid, budget, running_sum, out, scale=None,
+                                      pos=None, *, variant="l2", stream=None):
+    """The fused decode step without a workspace (see
+    ``vd_decode_attention_evict_noalloc`` in vd.h): the library's static device
+    scratch holds the split partials.  ``out`` is required (float32, q's
+    shape); nothing is allocated here."""
+    if out is None:
+        raise ValueError("out is required: the allocation-free call allocates nothing")
+    desc, n_h, b_h, out = _decode_args(k, v, q, n_valid, budget, running_sum, pos, out)
+    sc = float(v.shape[4]) ** -0.5 if scale is None else float(scale)
+    _check("vd_decode_attention_evict_noalloc", load().vd_decode_attention_evict_noalloc(
+        ctypes.byref(desc), _ptr(q), sc, _ptr(n_h), _ptr(b_h), VARIANTS[variant],
+        _ptr(running_sum), _ptr(pos), _ptr(out), _stream(v.device, stream)))
+    return out
+
+
+def vd_decode_attention_noalloc_max_bytes():
+    return int(load().vd_decode_attention_noalloc_max_bytes())
 
 
 def vd_stream_read(buf, sink, *, stream=None):
