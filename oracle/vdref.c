@@ -22,9 +22,20 @@
  *      evicted slots below N, ascending, receive the kept slots at or above N,
  *      ascending (the layout reading of "gather" used by this project).
  *
+ * Key-side scores (Sec. 4, Baselines, key geometry): the same three scores
+ * taken on the key rows instead of the value rows -- L2 on K (ManifoldKV),
+ * Dir on K (KeyDiff) and Norm on K (KeyNorm), the last keeping the SMALLEST
+ * norms (the opposite radial preference to the value-side Norm).
+ *
  * Decode attention of one query row (Sec. 2.1, Eq. attention; grouped-query
  * heads share a KV head): softmax of the scaled dot products with every cached
  * key, applied to the values, in fp64.
+ *
+ * FastCAOTE scores of one decode step (App. A, Eq. app_fastcaote; Sec. 4,
+ * Baselines): s_j = a_j / (1 - a_j) * ||v_j - v_bar||, where a_j is the
+ * observed attention weight of row j, taken as the mean over the G query
+ * heads of the KV head of their softmax weights (a reading: the paper does
+ * not say how grouped heads combine), and +infinity when a_j = 1.
  *
  * Geometry diagnostics of one unit (Sec. 3.1 and the bos-cosim equation of
  * Sec. 4), from their definitions: sigma_X = std_i ||x_i - x_bar|| for X = K
@@ -58,6 +69,9 @@
 #define VDREF_L2 0
 #define VDREF_DIR 1
 #define VDREF_NORM 2
+#define VDREF_KEY_L2 3
+#define VDREF_KEY_DIR 4
+#define VDREF_KEY_NORM 5
 
 #define VDREF_OK 0
 #define VDREF_BAD_ARG 1
@@ -107,13 +121,17 @@ int vdref_mean(const void *v, int dtype, int64_t n, int d, int64_t row_stride,
 
 /* ---- step 2: scores (Sec. 3.2) ----------------------------------------- */
 
+/* The rows `v` are the scored rows: value rows for the value-side scores,
+ * key rows for the key-side ones (which take the same three forms). */
 int vdref_score(const void *v, int dtype, int64_t n, int d, int64_t row_stride,
                 int variant, double *scores, double *mean_out)
 {
     if (n <= 0 || d <= 0 || !v || !scores)
         return VDREF_BAD_ARG;
-    if (variant != VDREF_L2 && variant != VDREF_DIR && variant != VDREF_NORM)
+    if (variant < VDREF_L2 || variant > VDREF_KEY_NORM)
         return VDREF_BAD_ARG;
+    if (variant >= VDREF_KEY_L2)
+        variant -= VDREF_KEY_L2;
 
     double *mean = (double *)malloc(sizeof(double) * (size_t)d);
     if (!mean)
@@ -210,6 +228,48 @@ int vdref_select_topn(const double *scores, int64_t n, int64_t N, uint8_t *keep)
     return VDREF_OK;
 }
 
+/* Lower score first; equal scores: lower index first. */
+static int by_score_asc_index_asc(const void *pa, const void *pb)
+{
+    const scored_index *a = (const scored_index *)pa;
+    const scored_index *b = (const scored_index *)pb;
+    if (a->s < b->s)
+        return -1;
+    if (a->s > b->s)
+        return 1;
+    if (a->j < b->j)
+        return -1;
+    if (a->j > b->j)
+        return 1;
+    return 0;
+}
+
+/* keep[j] = 1 for the N slots of smallest score (KeyNorm), ties to the lower index. */
+int vdref_select_smallest(const double *scores, int64_t n, int64_t N, uint8_t *keep)
+{
+    if (n < 0 || N < 1 || !keep || (n > 0 && !scores))
+        return VDREF_BAD_ARG;
+    if (n <= N) {
+        for (int64_t j = 0; j < n; ++j)
+            keep[j] = 1;
+        return VDREF_OK;
+    }
+    scored_index *order = (scored_index *)malloc(sizeof(scored_index) * (size_t)n);
+    if (!order)
+        return VDREF_BAD_ARG;
+    for (int64_t j = 0; j < n; ++j) {
+        order[j].s = scores[j];
+        order[j].j = j;
+    }
+    qsort(order, (size_t)n, sizeof(scored_index), by_score_asc_index_asc);
+    for (int64_t j = 0; j < n; ++j)
+        keep[j] = 0;
+    for (int64_t r = 0; r < N; ++r)
+        keep[order[r].j] = 1;
+    free(order);
+    return VDREF_OK;
+}
+
 /* ---- step 4: gather with slot reuse ------------------------------------ */
 
 static void copy_row(void *base, int dtype, int64_t row_stride, int d,
@@ -274,7 +334,10 @@ int vdref_evict_step(void *k, void *v, int dtype, int64_t U, int64_t cap, int d,
         return VDREF_BAD_ARG;
     if (dtype != VDREF_BF16 && dtype != VDREF_F32)
         return VDREF_BAD_ARG;
-    if (variant != VDREF_L2 && variant != VDREF_DIR && variant != VDREF_NORM)
+    if (variant < VDREF_L2 || variant > VDREF_KEY_NORM)
+        return VDREF_BAD_ARG;
+    int key_side = variant >= VDREF_KEY_L2;
+    if (key_side && !k)
         return VDREF_BAD_ARG;
     for (int64_t u = 0; u < U; ++u)
         if (n_unit[u] < 0 || n_unit[u] > cap || N_unit[u] < 1)
@@ -302,9 +365,13 @@ int vdref_evict_step(void *k, void *v, int dtype, int64_t U, int64_t cap, int d,
             status = VDREF_BAD_ARG;
             continue;
         }
-        vdref_score(vu, dtype, n, d, d, variant, su,
+        /* the scored rows: V, or K for a key-side score */
+        vdref_score(key_side ? ku : vu, dtype, n, d, d, variant, su,
                     mean_out ? mean_out + u * d : NULL);
-        vdref_select_topn(su, n, N, keepu);
+        if (variant == VDREF_KEY_NORM)
+            vdref_select_smallest(su, n, N, keepu);
+        else
+            vdref_select_topn(su, n, N, keepu);
         vdref_compact(ku, vu, dtype, n, N, d, d, keepu, pu);
         if (scores)
             memcpy(scores + u * cap, su, sizeof(double) * (size_t)n);
@@ -423,5 +490,56 @@ int vdref_attention(const double *q, const void *k, const void *v, int dtype, in
         out[c] = acc / den;
     }
     free(w);
+    return VDREF_OK;
+}
+
+/* ---- FastCAOTE scores of one decode step (App. A, Eq. app_fastcaote) -- */
+
+/*
+ * q: the G query rows of the KV head, [G][d] doubles; k, v: rows 0 .. n-1.
+ * a_j = (1/G) sum_g softmax_j(scale * q_g . k_j), the observed attention of
+ * row j averaged over the heads; scores[j] = a_j / (1 - a_j) * ||v_j - v_bar||
+ * with v_bar the mean of the n value rows; +infinity where a_j = 1.
+ */
+int vdref_fastcaote_scores(const double *q, int G, const void *k, const void *v, int dtype,
+                           int64_t n, int d, int64_t row_stride, double scale, double *scores)
+{
+    if (n <= 0 || d <= 0 || G < 1 || !q || !k || !v || !scores)
+        return VDREF_BAD_ARG;
+    double *a = (double *)calloc((size_t)n, sizeof(double));
+    double *w = (double *)malloc(sizeof(double) * (size_t)n);
+    double *dist = (double *)malloc(sizeof(double) * (size_t)n);
+    if (!a || !w || !dist) {
+        free(a);
+        free(w);
+        free(dist);
+        return VDREF_BAD_ARG;
+    }
+    for (int g = 0; g < G; ++g) {
+        /* softmax of head g over the n rows, the largest logit subtracted first */
+        double top = -INFINITY;
+        for (int64_t j = 0; j < n; ++j) {
+            double dot = 0.0;
+            for (int c = 0; c < d; ++c)
+                dot += q[g * d + c] * get_elem(k, dtype, j * row_stride + c);
+            w[j] = scale * dot;
+            if (w[j] > top)
+                top = w[j];
+        }
+        double den = 0.0;
+        for (int64_t j = 0; j < n; ++j) {
+            w[j] = exp(w[j] - top);
+            den += w[j];
+        }
+        for (int64_t j = 0; j < n; ++j)
+            a[j] += w[j] / den / (double)G;
+    }
+    /* the distances of the value rows to their mean (the L2 scores) */
+    vdref_score(v, dtype, n, d, row_stride, VDREF_L2, dist, NULL);
+    for (int64_t j = 0; j < n; ++j)
+        scores[j] = a[j] < 1.0 ? a[j] / (1.0 - a[j]) * dist[j] : INFINITY;
+    free(a);
+    free(w);
+    free(dist);
     return VDREF_OK;
 }

@@ -17,7 +17,11 @@ F32 = 1
 L2 = 0
 DIR = 1
 NORM = 2
-VARIANTS = {"l2": L2, "dir": DIR, "norm": NORM}
+KEY_L2 = 3
+KEY_DIR = 4
+KEY_NORM = 5
+VARIANTS = {"l2": L2, "dir": DIR, "norm": NORM, "key_l2": KEY_L2, "key_dir": KEY_DIR,
+            "key_norm": KEY_NORM}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvdref.so")
@@ -56,13 +60,17 @@ class Oracle:
         lib.vdref_mean.argtypes = [_p, _i32, _i64, _i32, _i64, _p]
         lib.vdref_score.argtypes = [_p, _i32, _i64, _i32, _i64, _i32, _p, _p]
         lib.vdref_select_topn.argtypes = [_p, _i64, _i64, _p]
+        lib.vdref_select_smallest.argtypes = [_p, _i64, _i64, _p]
+        lib.vdref_fastcaote_scores.argtypes = [_p, _i32, _p, _p, _i32, _i64, _i32, _i64,
+                                               ctypes.c_double, _p]
         lib.vdref_compact.argtypes = [_p, _p, _i32, _i64, _i64, _i32, _i64, _p, _p]
         lib.vdref_evict_step.argtypes = [_p, _p, _i32, _i64, _i64, _i32, _p, _p, _i32,
                                          _p, _p, _p, _p, _i32]
         lib.vdref_geometry.argtypes = [_p, _p, _i32, _i64, _i32, _i64, _p]
         lib.vdref_attention.argtypes = [_p, _p, _p, _i32, _i64, _i32, _i64, ctypes.c_double, _p]
         for f in ("vdref_mean", "vdref_score", "vdref_select_topn", "vdref_compact",
-                  "vdref_evict_step", "vdref_geometry", "vdref_attention"):
+                  "vdref_evict_step", "vdref_geometry", "vdref_attention",
+                  "vdref_select_smallest", "vdref_fastcaote_scores"):
             getattr(lib, f).restype = ctypes.c_int
         self.lib = lib
         self.path = path
@@ -84,7 +92,8 @@ class Oracle:
         return out
 
     def score(self, v: np.ndarray, variant="l2"):
-        """(scores [n], mean [d]) of the rows of ``v`` ([n, d])."""
+        """(scores [n], mean [d]) of the rows of ``v`` ([n, d]): the value rows
+        for a value-side variant, the key rows for a key-side one."""
         v = np.ascontiguousarray(v)
         n, d = v.shape
         s = np.empty(n, np.float64)
@@ -102,6 +111,31 @@ class Oracle:
         if self.lib.vdref_select_topn(_ptr(scores), n, N, _ptr(keep)):
             raise ValueError("vdref_select_topn rejected its arguments")
         return keep
+
+    def select_smallest(self, scores: np.ndarray, N: int) -> np.ndarray:
+        """Keep mask (uint8 [n]) of the N lowest scores, ties to the lower index."""
+        scores = np.ascontiguousarray(scores, dtype=np.float64)
+        n = scores.shape[0]
+        keep = np.empty(n, np.uint8)
+        if self.lib.vdref_select_smallest(_ptr(scores), n, N, _ptr(keep)):
+            raise ValueError("vdref_select_smallest rejected its arguments")
+        return keep
+
+    def fastcaote_scores(self, q: np.ndarray, k: np.ndarray, v: np.ndarray,
+                         scale: float) -> np.ndarray:
+        """FastCAOTE scores (float64 [n]) of one decode step: q [G, d] (the
+        query rows of the KV head, any float dtype, taken as fp64), k and v
+        [n, d]."""
+        k, v = np.ascontiguousarray(k), np.ascontiguousarray(v)
+        q = np.ascontiguousarray(np.atleast_2d(q), dtype=np.float64)
+        if k.shape != v.shape or k.dtype != v.dtype or q.shape[1] != v.shape[1]:
+            raise ValueError("q [G, d], k and v [n, d] of one dtype")
+        n, d = v.shape
+        out = np.empty(n, np.float64)
+        if self.lib.vdref_fastcaote_scores(_ptr(q), q.shape[0], _ptr(k), _ptr(v), _dtype_tag(v),
+                                           n, d, d, float(scale), _ptr(out)):
+            raise ValueError("vdref_fastcaote_scores rejected its arguments")
+        return out
 
     def compact(self, k, v, n: int, N: int, keep: np.ndarray, pos=None):
         """Slot-reuse gather, in place, on [>=n, d] arrays ``k`` and ``v``."""
@@ -208,6 +242,14 @@ def evict_step(k, v, n_unit, N_unit, variant="l2", pos=None, nthreads=0):
 
 def geometry(k, v):
     return load().geometry(k, v)
+
+
+def select_smallest(scores, N):
+    return load().select_smallest(scores, N)
+
+
+def fastcaote_scores(q, k, v, scale):
+    return load().fastcaote_scores(q, k, v, scale)
 
 
 def attention(q, k, v, scale):

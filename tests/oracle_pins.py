@@ -19,6 +19,13 @@ Pins and what they fix:
   attention           decode attention (Sec. 2.1, Eq. attention): zero query = mean,
                       one row, hand weights 1/4 and 3/4, scale, overflow-free one-hot,
                       key shift, permutation, bf16
+  key side            the three scores on the key rows (Sec. 4, Baselines): hand kept
+                      sets with values that would keep other sets, KeyNorm keeping the
+                      smallest norms, the law of cosines on K, K and V moved together
+  FastCAOTE           App. A, Eq. app_fastcaote: uniform attention collapses to the
+                      L2 score / (n - 1) (App. A, the max-entropy limit), hand values
+                      with weights 1/4 and 3/4 and a two-head mean, one-hot, key shift,
+                      permutation, scale, bf16
 """
 import itertools
 import json
@@ -427,12 +434,115 @@ def check_attention(orc):
     assert _rel_close(orc.attention(q, kb, vb, 0.5), orc.attention(q, kf, vf, 0.5), 1e-12, 1e-15)
 
 
+def check_key_side(orc):
+    """Key-side scores (Sec. 4, Baselines, key geometry): L2, Dir and Norm on
+    the key rows, KeyNorm keeping the smallest norms, through the batched pass.
+    K holds W1's rows (scores: L2 [r2, 1, 1, 2 r2], Dir [1, 1-1/r2, 1-1/r2, 0],
+    norms [0, 1, 1, 3 r2]); the value rows would keep other sets."""
+    K = _f32([[0, 0], [1, 0], [0, 1], [3, 3]])
+    V = _f32([[1, 1], [1, 1], [0, 0], [1, 1]])
+    r2 = np.sqrt(2.0)
+    want_s = {"key_l2": [r2, 1, 1, 2 * r2], "key_dir": [1, 1 - 1 / r2, 1 - 1 / r2, 0],
+              "key_norm": [0, 1, 1, 3 * r2]}
+    want_keep = {("key_l2", 2): [0, 3], ("key_l2", 3): [0, 1, 3], ("key_dir", 2): [0, 1],
+                 ("key_dir", 3): [0, 1, 2], ("key_norm", 2): [0, 1], ("key_norm", 3): [0, 1, 2]}
+    for (var, N), want in want_keep.items():
+        k, v = K[None].copy(), V[None].copy()
+        pos = np.arange(4, dtype=np.int32)[None].copy()
+        s, keep, _ = orc.evict_step(k, v, [4], [N], var, pos=pos)
+        assert _rel_close(s[0, :4], want_s[var], 1e-12, 1e-12), (var, s[0, :4])
+        assert _kept_list(keep[0, :4]) == want, (var, N, _kept_list(keep[0, :4]))
+        for slot in range(N):   # K and V rows stay paired with their slot id
+            assert np.array_equal(k[0, slot], K[pos[0, slot]]), (var, N)
+            assert np.array_equal(v[0, slot], V[pos[0, slot]]), (var, N)
+    # KeyNorm: n = N + 1 evicts the largest norm, the highest slot among equals
+    k = _f32([[3, 4], [0, 1], [4, 3], [1, 0]])[None].copy()
+    _, keep, _ = orc.evict_step(k, k.copy(), [4], [3], "key_norm")
+    assert _kept_list(keep[0, :4]) == [0, 1, 3]
+    # law of cosines on K (Sec. 3.2, Eq. decomp on the key side), random rows
+    rng = np.random.default_rng(51)
+    for trial in range(10):
+        n, d = int(rng.integers(3, 40)), int(rng.choice([2, 5, 16]))
+        k = _f32(rng.standard_normal((1, n, d)) + rng.normal(0, 2, d))
+        v = _f32(rng.standard_normal((1, n, d)) * 3.0)
+        out = {var: orc.evict_step(k.copy(), v.copy(), [n], [n], var)
+               for var in ("key_l2", "key_dir", "key_norm")}
+        s2, sd, sn = out["key_l2"][0][0, :n], out["key_dir"][0][0, :n], out["key_norm"][0][0, :n]
+        mn = np.sqrt((out["key_l2"][2][0] ** 2).sum())
+        rhs = sn ** 2 - 2.0 * sn * mn * (1.0 - sd) + mn ** 2
+        assert np.all(np.abs(s2 ** 2 - rhs) <= 1e-11 * (sn ** 2 + mn ** 2).max()), trial
+        assert _rel_close(out["key_l2"][2][0], k[0].astype(np.float64).mean(axis=0), 1e-12, 1e-14)
+
+
+def check_fastcaote(orc):
+    """FastCAOTE, s_j = a_j / (1 - a_j) * ||v_j - v_bar|| (App. A, Eq.
+    app_fastcaote), a_j the softmax weight of row j averaged over the heads."""
+    rng = np.random.default_rng(61)
+    # uniform attention (zero queries): a_j = 1/n, so s_j = ||v_j - v_bar|| / (n - 1),
+    # the ValueDiff score up to a factor that leaves its ranking unchanged (App. A)
+    for n, G in ((2, 1), (7, 3), (40, 4)):
+        k = _f32(rng.standard_normal((n, 5)))
+        v = _f32(rng.standard_normal((n, 5)) * 2.0 + 1.0)
+        s = orc.fastcaote_scores(np.zeros((G, 5)), k, v, 0.3)
+        l2, _ = orc.score(v, "l2")
+        assert _rel_close(s, l2 / (n - 1), 1e-12, 1e-15), (n, G)
+    # two rows, logits 0 and ln 3: weights 1/4 and 3/4, ratios 1/3 and 3; the
+    # values (0,0) and (2,0) lie at distance 1 from their mean (1,0)
+    K = _f32([[0, 0], [1, 0]])
+    V = _f32([[0, 0], [2, 0]])
+    q1 = np.array([[np.log(3.0), 0.0]])
+    assert _rel_close(orc.fastcaote_scores(q1, K, V, 1.0), [1 / 3, 3.0], 1e-12)
+    # two heads, uniform and (1/4, 3/4): mean weights 3/8 and 5/8, ratios 3/5 and 5/3
+    q2 = np.array([[0.0, 0.0], [np.log(3.0), 0.0]])
+    assert _rel_close(orc.fastcaote_scores(q2, K, V, 1.0), [0.6, 5 / 3], 1e-12)
+    # one logit 1000 above the rest: that row takes all the weight (+inf), the others none
+    kk = np.zeros((5, 4), np.float32)
+    kk[2, 0] = 1.0
+    vv = _f32(rng.standard_normal((5, 4)))
+    s = orc.fastcaote_scores(np.array([[1000.0, 0, 0, 0]]), kk, vv, 1.0)
+    assert np.isinf(s[2]) and s[2] > 0 and np.all(s[[0, 1, 3, 4]] == 0.0), s
+    # logits near 800 (past fp64's exp range) give the weights of the same
+    # logits less 800 (offsets in sixteenths: exact in fp32)
+    off = _f32(np.zeros((12, 3)))
+    off[:, 0] = rng.integers(0, 48, 12) / 16.0
+    hi = _f32(off + np.array([800.0, 0, 0], np.float32))
+    vv = _f32(rng.standard_normal((12, 3)))
+    qq = np.array([[1.0, 0.3, -0.2]])
+    s_hi = orc.fastcaote_scores(qq, hi, vv, 1.0)
+    assert np.all(np.isfinite(s_hi)), s_hi
+    assert _rel_close(s_hi, orc.fastcaote_scores(qq, off, vv, 1.0), 1e-12, 1e-15)
+    # the scale multiplies the logits
+    q = rng.standard_normal((2, 6)) * 0.5
+    kx = _f32(rng.standard_normal((20, 6)))
+    vx = _f32(rng.standard_normal((20, 6)))
+    a = orc.fastcaote_scores(q, kx, vx, 0.7)
+    assert _rel_close(a, orc.fastcaote_scores(0.7 * q, kx, vx, 1.0), 1e-12, 1e-15)
+    assert not _rel_close(a, orc.fastcaote_scores(q, kx, vx, 1.0), 1e-6)
+    # invariances: a common key shift (integer keys: exact), rows permuted
+    # together, values scaled by a (scores scale by |a|)
+    ki = _f32(rng.integers(-3, 4, (30, 6)))
+    vi = _f32(rng.standard_normal((30, 6)))
+    s0 = orc.fastcaote_scores(q, ki, vi, 0.4)
+    ks = _f32(ki + rng.integers(-2, 3, 6))
+    assert _rel_close(orc.fastcaote_scores(q, ks, vi, 0.4), s0, 1e-10, 1e-15)
+    perm = rng.permutation(30)
+    assert _rel_close(orc.fastcaote_scores(q, ki[perm], vi[perm], 0.4), s0[perm], 1e-12, 1e-15)
+    assert _rel_close(orc.fastcaote_scores(q, ki, _f32(vi * -2.0), 0.4), 2.0 * s0, 1e-12, 1e-15)
+    # bf16 rows give the scores of their fp32 values
+    kb = (ki.view(np.uint32) >> 16).astype(np.uint16)
+    vb = (vi.view(np.uint32) >> 16).astype(np.uint16)
+    kf = _f32((kb.astype(np.uint32) << 16).view(np.float32))
+    vf = _f32((vb.astype(np.uint32) << 16).view(np.float32))
+    assert _rel_close(orc.fastcaote_scores(q, kb, vb, 0.4), orc.fastcaote_scores(q, kf, vf, 0.4),
+                      1e-12, 1e-15)
+
+
 ALL_CHECKS = [
     check_decode, check_mean_library, check_worked_examples,
     check_minimal_disturbance, check_law_of_cosines, check_dirichlet,
     check_invariances, check_select_vs_sort, check_select_bruteforce,
     check_select_special, check_compact, check_evict_step_batch, check_geometry,
-    check_attention,
+    check_attention, check_key_side, check_fastcaote,
 ]
 
 

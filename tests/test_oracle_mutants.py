@@ -34,11 +34,12 @@ MUTANTS = [
      "double cosv = denom > 0.0 ? dot / denom : 1.0;"),
     ("dir_uses_squared_norm", "double denom = sqrt(vn2) * mean_norm;",
      "double denom = vn2 * mean_norm;"),
-    ("tie_keeps_higher_index", "if (a->j < b->j)\n        return -1;",
-     "if (a->j < b->j)\n        return 1;"),
+    ("tie_keeps_higher_index", "if (a->s < b->s)\n        return 1;\n    if (a->j < b->j)\n        return -1;",
+     "if (a->s < b->s)\n        return 1;\n    if (a->j < b->j)\n        return 1;"),
     ("keeps_lowest_scores", "if (a->s > b->s)\n        return -1;\n    if (a->s < b->s)\n        return 1;",
      "if (a->s > b->s)\n        return 1;\n    if (a->s < b->s)\n        return -1;"),
-    ("keeps_one_too_few", "for (int64_t r = 0; r < N; ++r)", "for (int64_t r = 0; r < N - 1; ++r)"),
+    ("keeps_one_too_few", "by_score_desc_index_asc);\n    for (int64_t j = 0; j < n; ++j)\n        keep[j] = 0;\n    for (int64_t r = 0; r < N; ++r)",
+     "by_score_desc_index_asc);\n    for (int64_t j = 0; j < n; ++j)\n        keep[j] = 0;\n    for (int64_t r = 0; r < N - 1; ++r)"),
     ("movers_start_past_budget", "int64_t next_mover = N;", "int64_t next_mover = N + 1;"),
     ("pos_not_moved", "pos[hole] = pos[next_mover];", "pos[hole] = pos[hole];"),
     ("k_not_moved", "if (k)\n            copy_row(k,", "if (0)\n            copy_row(k,"),
@@ -51,13 +52,27 @@ MUTANTS = [
      "for (int64_t i = 0; i < n; ++i)\n                m +="),
     ("sigma_k_of_v", "dispersion(k, dtype, n, d, row_stride, &out[2], &out[0]);",
      "dispersion(v, dtype, n, d, row_stride, &out[2], &out[0]);"),
-    ("attn_no_max_shift", "w[j] = exp(w[j] - top);", "w[j] = exp(w[j]);"),
-    ("attn_ignores_scale", "w[j] = scale * dot;", "w[j] = dot;"),
+    ("attn_no_max_shift", "\n        w[j] = exp(w[j] - top);", "\n        w[j] = exp(w[j]);"),
+    ("attn_ignores_scale", "\n        w[j] = scale * dot;", "\n        w[j] = dot;"),
     ("attn_divides_by_n", "out[c] = acc / den;", "out[c] = acc / (double)n;"),
     ("attn_same_key_for_all", "dot += q[c] * get_elem(k, dtype, j * row_stride + c);",
      "dot += q[c] * get_elem(k, dtype, c);"),
     ("attn_values_from_keys", "acc += w[j] * get_elem(v, dtype, j * row_stride + c);",
      "acc += w[j] * get_elem(k, dtype, j * row_stride + c);"),
+    ("key_side_scores_values", "vdref_score(key_side ? ku : vu, dtype",
+     "vdref_score(vu, dtype"),
+    ("key_norm_keeps_largest", "if (variant == VDREF_KEY_NORM)\n            vdref_select_smallest",
+     "if (0)\n            vdref_select_smallest"),
+    ("key_variant_maps_to_next_form", "variant -= VDREF_KEY_L2;", "variant -= VDREF_KEY_L2 - 1;"),
+    ("smallest_tie_keeps_higher_index",
+     "if (a->s > b->s)\n        return 1;\n    if (a->j < b->j)\n        return -1;",
+     "if (a->s > b->s)\n        return 1;\n    if (a->j < b->j)\n        return 1;"),
+    ("fastcaote_ratio_dropped", "? a[j] / (1.0 - a[j]) * dist[j]", "? a[j] * dist[j]"),
+    ("fastcaote_heads_summed", "a[j] += w[j] / den / (double)G;", "a[j] += w[j] / den;"),
+    ("fastcaote_no_max_shift", "w[j] = exp(w[j] - top);\n            den += w[j];",
+     "w[j] = exp(w[j]);\n            den += w[j];"),
+    ("fastcaote_ignores_scale", "w[j] = scale * dot;\n            if (w[j] > top)\n                top = w[j];\n        }\n        double den",
+     "w[j] = dot;\n            if (w[j] > top)\n                top = w[j];\n        }\n        double den"),
 ]
 
 
