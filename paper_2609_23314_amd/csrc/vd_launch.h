@@ -23,8 +23,9 @@ struct LdsHead {
     uint32_t hist[kBins]; // selection histogram
     uint32_t cand_key[kCand];
     uint32_t cand_idx[kCand];
-    float mean[256];      // fp32 mean used for scoring
-    float udir[256];      // mean / ||mean|| (direction variant)
+    float mean[256];      // fp32 mean used for scoring (its high part for L2)
+    float aux[256];       // L2: the low part of the mean (mean - high part);
+                          // Dir: mean / ||mean||
     double sum[256];      // fp64 column sums of all n rows
     double old_sum[256];  // fp64 column sums of the rows the state covered
 };
@@ -59,12 +60,15 @@ struct UnitParams {
     const uint8_t *keep_in;   // compact kernel input
     float *mean_out;          // [U][D] or null
     double *geom_out;         // [U][5] (geometry kernel)
+    const double *k_sum;      // geometry: [U][D+1] column sums of K and their row count, or null
+    const double *v_sum;      // geometry: the same for V, or null
     // fused decode attention
     const float *q;           // [S][L][Hq][D] of the launch's first sequence
     float *attn_out;          // [S][L][Hq][D]
     float *ws_acc;            // [U][splits][G][D] partial outputs (unnormalised)
     float *ws_ml;             // [U][splits][G][2] partial max logit (log2 units) and weight sum
     unsigned long long *ws_amin;  // [U][splits] (key << 32 | ~slot) of the lowest score
+    float *ws_rows;           // FastCAOTE: [U][capacity][G + 1] log2 logits of the G heads, distance
     int32_t splits, split_rows;   // row splits per unit and rows per split
     float qscale;             // softmax scale times log2(e)
     int32_t pad1;
@@ -82,7 +86,7 @@ hipError_t launch_compact(const UnitParams &p, int num_seqs, int dtype, int head
 // then the combine kernel (grid heads x seqs*layers); G = query heads per KV head.
 constexpr int kAttnThreads = 256;
 hipError_t launch_attn(const UnitParams &p, int num_seqs, int dtype, int head_dim, int group,
-                       size_t split_lds, hipStream_t stream);
+                       bool caote, size_t split_lds, hipStream_t stream);
 hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int head_dim,
                            size_t lds_bytes, hipStream_t stream);
 // Static device scratch of the allocation-free fused decode step (one copy per
@@ -91,6 +95,9 @@ hipError_t launch_geometry(const UnitParams &p, int num_seqs, int dtype, int hea
 constexpr size_t kScratchBytes = size_t(32) << 20;
 constexpr int kMaxDevices = 64;
 hipError_t scratch_memory(hipStream_t stream, void **ptr);
+// Debug builds (VD_DEBUG=1): waits for the device, then returns and clears the
+// word in which the kernels' LDS index checks set one bit per failing site.
+hipError_t debug_take_error_word(unsigned int *out);
 // Reads n16 16-byte words once over the whole GPU (a measurement aid).
 hipError_t launch_stream_read(const void *buf, size_t n16, uint32_t *sink, hipStream_t stream);
 

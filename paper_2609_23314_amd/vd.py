@@ -74,7 +74,7 @@ def load():
     lib.vd_status_string.restype = ctypes.c_char_p
     lib.vd_stream_read.argtypes = [P, SZ, P, P]
     lib.vd_stream_read.restype = ctypes.c_int
-    lib.vd_geometry.argtypes = [D, P, P, P]
+    lib.vd_geometry.argtypes = [D, P, P, P, P, P]
     lib.vd_geometry.restype = ctypes.c_int
     lib.vd_decode_attention_evict.argtypes = [D, P, ctypes.c_float, P, P, I32, P, P, P, P, SZ, P]
     lib.vd_decode_attention_evict.restype = ctypes.c_int
@@ -221,11 +221,12 @@ def vd_evict_step(k, v, n_valid, budget, variant="l2", running_sum=None, pos=Non
         _stream(v.device, stream)))
 
 
-def vd_geometry(k, v, n_valid, out=None, *, stream=None):
+def vd_geometry(k, v, n_valid, out=None, *, k_sum=None, v_sum=None, stream=None):
     """Key and value geometry of every unit (see ``vd_geometry`` in vd.h):
     float64 [U, 5] = sigma_K, sigma_V, mean ||k - k_bar||, mean ||v - v_bar||,
-    bos-cosim."""
-    U = _units(v)
+    bos-cosim.  k_sum / v_sum: optional float64 [U, D + 1] column sums and
+    row counts (both or neither)."""
+    U, Dh = _units(v), v.shape[4]
     if k is None:
         raise ValueError("vd_geometry needs k")
     desc = cache_desc(v, k)
@@ -233,8 +234,11 @@ def vd_geometry(k, v, n_valid, out=None, *, stream=None):
     if out is None:
         out = torch.empty((U, 5), dtype=torch.float64, device=v.device)
     _need(out, "out", torch.float64, U * 5, v.device)
-    _check("vd_geometry", load().vd_geometry(ctypes.byref(desc), _ptr(n_h), _ptr(out),
-                                             _stream(v.device, stream)))
+    for t, nm in ((k_sum, "k_sum"), (v_sum, "v_sum")):
+        if t is not None:
+            _need(t, nm, torch.float64, U * (Dh + 1), v.device)
+    _check("vd_geometry", load().vd_geometry(ctypes.byref(desc), _ptr(n_h), _ptr(k_sum),
+                                             _ptr(v_sum), _ptr(out), _stream(v.device, stream)))
     return out
 
 

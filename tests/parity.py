@@ -12,10 +12,12 @@ Bar (per unit):
               the rows the GPU kept, in the slot-reuse layout.
   scores      |s_gpu - s_ref| <= rtol * s_ref + atol, rtol = 1e-3 (bf16) or
               1e-5 (fp32), atol = 1e-6 * max(max_j s_ref, scale), where scale is
-              1 for Dir (1 - cos is dimensionless, at most 2), the largest row
-              norm for L2 (fp32 cancellation in v_j - v_bar grows with |v|)
-              and 0 for Norm.
-  state       the running sum equals the fp64 sum of the kept value rows.
+              1 for Dir (1 - cos is dimensionless, at most 2) and 0 for L2 and
+              Norm.  (The kernels subtract the mean as a pair of fp32 numbers,
+              so an L2 score keeps fp32 accuracy relative to itself however
+              far the mean lies from the origin.)
+  state       the running sum equals the fp64 sum of the kept rows of the
+              scored tensor (V; K for a key-side score).
 """
 import numpy as np
 import torch
@@ -68,11 +70,7 @@ class Report:
 
 def score_scale(rows, variant):
     """The `scale` of the score tolerance for one unit's rows (oracle form)."""
-    if variant == "dir":
-        return 1.0
-    if variant == "l2" and rows.size:
-        return float(np.sqrt((values_f64(rows) ** 2).sum(axis=-1)).max())
-    return 0.0
+    return 1.0 if variant in ("dir", "key_dir") else 0.0
 
 
 def check_scores(s_gpu, s_ref, dtype, what="", scale=0.0):
@@ -87,15 +85,16 @@ def check_scores(s_gpu, s_ref, dtype, what="", scale=0.0):
     return float((err / np.maximum(np.abs(s_ref), atol + 1e-300)).max()) if s_ref.size else 0.0
 
 
-def keep_agrees(keep_gpu, keep_ref, s_ref, N, what="", scale=0.0):
-    """True if identical; False for a tolerated near-tie; asserts otherwise."""
+def keep_agrees(keep_gpu, keep_ref, s_ref, N, what="", scale=0.0, smallest=False):
+    """True if identical; False for a tolerated near-tie; asserts otherwise.
+    `smallest`: the N lowest scores are kept (KeyNorm)."""
     keep_gpu = np.asarray(keep_gpu).astype(bool)
     keep_ref = np.asarray(keep_ref).astype(bool)
     if np.array_equal(keep_gpu, keep_ref):
         return True
     n = keep_ref.size
     assert keep_gpu.sum() == min(N, n), f"{what}: GPU kept {keep_gpu.sum()} of {n}, budget {N}"
-    s_sorted = np.sort(s_ref)[::-1]
+    s_sorted = np.sort(s_ref) if smallest else np.sort(s_ref)[::-1]
     s_N = s_sorted[min(N, n) - 1]
     band = REL_TIE * abs(s_N) + 1e-6 * max(np.abs(s_ref).max(), scale)
     diff = np.flatnonzero(keep_gpu != keep_ref)
@@ -142,13 +141,16 @@ def compare_pass(orc, pre_k, pre_v, post_k, post_v, n_unit, N_unit, variant, dty
         report.units += 1
         if n == 0:
             continue
-        scale = score_scale(pre_v[i, :n], variant)
+        key_side = variant.startswith("key")
+        scored_pre = pre_k if key_side else pre_v
+        scored_post = post_k if key_side else post_v
+        scale = score_scale(scored_pre[i, :n], variant)
         if scores_gpu is not None:
             e = check_scores(scores_gpu[i, :n], ref_scores[i, :n], dtype, what, scale)
             report.max_score_err = max(report.max_score_err, e)
         if keep_gpu is not None:
             same = keep_agrees(keep_gpu[i, :n], ref_keep[i, :n], ref_scores[i, :n], N, what,
-                               scale)
+                               scale, smallest=variant == "key_norm")
             kept = keep_gpu[i, :n]
         else:
             same = True
@@ -168,10 +170,10 @@ def compare_pass(orc, pre_k, pre_v, post_k, post_v, n_unit, N_unit, variant, dty
                 check_layout(post_k[i], pre_k[i], kept, n, N, what + " K")
             if pre_pos is not None:
                 check_layout(post_pos[i], pre_pos[i], kept, n, N, what + " pos")
-        if state is not None:
-            want = values_f64(post_v[i, :m]).sum(axis=0)
+        if state is not None:   # the sum of the kept rows of the scored tensor
+            want = values_f64(scored_post[i, :m]).sum(axis=0)
             got = state[i, :-1]
             assert state[i, -1] == m, f"{what}: state count {state[i, -1]} != {m}"
-            tol = 1e-12 * np.abs(values_f64(post_v[i, :m])).sum(axis=0) + 1e-300
+            tol = 1e-12 * np.abs(values_f64(scored_post[i, :m])).sum(axis=0) + 1e-300
             assert np.all(np.abs(got - want) <= tol), f"{what}: running sum differs"
     return report

@@ -33,6 +33,16 @@ def test_library_exports_every_declared_symbol():
     lib = ctypes.CDLL(vd.LIB_PATH)
     for name in declared_functions():
         assert hasattr(lib, name), name
+    assert not hasattr(lib, "vd_debug_take_error_word")   # the release build has no checks
+
+
+def test_debug_library_exports_every_declared_symbol():
+    from paper_2609_23314_amd import build as lib_build
+    lib = ctypes.CDLL(lib_build.DEBUG_LIB)
+    for name in declared_functions() + ["vd_debug_take_error_word"]:
+        assert hasattr(lib, name), name
+    lib.vd_debug_take_error_word.argtypes = [ctypes.c_void_p]
+    assert lib.vd_debug_take_error_word(None) == vd.VD_ERR_INVALID_ARG
 
 
 def good_desc(**kw):
@@ -79,12 +89,23 @@ def test_descriptor_rejected(field, value, status):
     assert call_step(good_desc(**{field: value})) == status
 
 
+def n_arr_2():
+    return (ctypes.c_int32 * 2)(5, 5)
+
+
 def test_counts_rejected():
     d = good_desc()
     assert call_step(d, n=(101, 5)) == vd.VD_ERR_INVALID_ARG    # n > capacity
     assert call_step(d, n=(-1, 5)) == vd.VD_ERR_INVALID_ARG
     assert call_step(d, N=(0, 5)) == vd.VD_ERR_INVALID_ARG      # budget < 1
-    assert call_step(d, variant=3) == vd.VD_ERR_INVALID_ARG
+    assert call_step(d, variant=7) == vd.VD_ERR_INVALID_ARG
+    assert call_step(d, variant=6) == vd.VD_ERR_INVALID_ARG          # FastCAOTE: decode step only
+    nok = good_desc()
+    nok.k = None
+    for key_variant in (3, 4, 5):                                     # key-side scores need K
+        assert call_step(nok, variant=key_variant) == vd.VD_ERR_INVALID_ARG
+        assert vd.load().vd_score(ctypes.byref(nok), n_arr_2(), key_variant, FAKE_V, None,
+                                  None) == vd.VD_ERR_INVALID_ARG
     assert call_step(d, rs=ctypes.c_void_p(0x1004)) == vd.VD_ERR_INVALID_ARG  # misaligned state
     lib = vd.load()
     n_arr = (ctypes.c_int32 * 2)(5, 5)
@@ -120,17 +141,23 @@ def test_geometry_rejects_bad_arguments():
     lib = vd.load()
     n_arr = (ctypes.c_int32 * 2)(5, 5)
     out = ctypes.c_void_p(0x7F0000000000)
+    sums = ctypes.c_void_p(0x7F0000200000)
     d = good_desc()
     d.k = None                                   # K is required
-    assert lib.vd_geometry(ctypes.byref(d), n_arr, out, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, None, out, None) == vd.VD_ERR_INVALID_ARG
     d = good_desc()
-    assert lib.vd_geometry(ctypes.byref(d), None, out, None) == vd.VD_ERR_INVALID_ARG
-    assert lib.vd_geometry(ctypes.byref(d), (ctypes.c_int32 * 2)(101, 5), out,
+    assert lib.vd_geometry(ctypes.byref(d), None, None, None, out, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), (ctypes.c_int32 * 2)(101, 5), None, None, out,
                            None) == vd.VD_ERR_INVALID_ARG            # n > capacity
-    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, None) == vd.VD_ERR_INVALID_ARG
-    assert lib.vd_geometry(ctypes.byref(d), n_arr, ctypes.c_void_p(0x7F0000000004),
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, None, None, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, None, ctypes.c_void_p(0x7F0000000004),
                            None) == vd.VD_ERR_INVALID_ARG            # misaligned out
-    assert lib.vd_geometry(ctypes.byref(good_desc(head_dim=96)), n_arr, out,
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, sums, None, out,
+                           None) == vd.VD_ERR_INVALID_ARG            # one sum without the other
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, None, sums, out, None) == vd.VD_ERR_INVALID_ARG
+    assert lib.vd_geometry(ctypes.byref(d), n_arr, sums, ctypes.c_void_p(0x7F0000200004), out,
+                           None) == vd.VD_ERR_INVALID_ARG            # misaligned sum
+    assert lib.vd_geometry(ctypes.byref(good_desc(head_dim=96)), n_arr, None, None, out,
                            None) == vd.VD_ERR_UNSUPPORTED
 
 

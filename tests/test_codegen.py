@@ -24,14 +24,25 @@ CSRC = os.path.join(ROOT, "paper_2609_23314_amd", "csrc")
 MAX_PRIVATE_BYTES = 0    # per lane
 
 
-@pytest.fixture(scope="module")
-def kernels(tmp_path_factory):
+def _assembly(tmp_path_factory, defines=()):
     out = tmp_path_factory.mktemp("asm") / "vd_kernels.s"
     cmd = [lib_build.hipcc(), f"--offload-arch={lib_build.ARCH}", "--cuda-device-only", "-S",
-           "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+           "-O3", "-std=c++17", "-I", os.path.join(ROOT, "include"), "-I", CSRC, *defines,
            *lib_build.DEVICE_FLAGS, os.path.join(CSRC, "vd_kernels.hip"), "-o", str(out)]
     subprocess.run(cmd, check=True, capture_output=True)
-    text = out.read_text()
+    return out.read_text()
+
+
+def _kernel_body(text, part):
+    """Assembly of the first kernel whose symbol contains `part`."""
+    m = re.search(r"^(_Z\S*" + part + r"\S*):\s*;\s*@", text, flags=re.M)
+    assert m, part
+    return text[m.end():text.find(".end_amdhsa_kernel", m.end())]
+
+
+@pytest.fixture(scope="module")
+def kernels(tmp_path_factory):
+    text = _assembly(tmp_path_factory)
     # split into functions: "name:" label lines that open a function body
     bodies = {}
     for m in re.finditer(r"^(_Z\S+):\s*;\s*@", text, flags=re.M):
@@ -63,3 +74,13 @@ def test_no_stack_frame(kernels):
     assert sizes, "no kernel descriptors found"
     big = {k: v for k, v in sizes.items() if v > MAX_PRIVATE_BYTES}
     assert not big, big
+
+
+def test_lds_checks_only_in_the_debug_build(kernels, tmp_path_factory):
+    """The debug build's LDS index checks are compiled in (they record a
+    violation with a global atomic OR), and the release build has none."""
+    text, _, _ = kernels
+    assert "global_atomic_or" not in _kernel_body(text, "step_kernel")
+    dbg = _assembly(tmp_path_factory, ["-DVD_DEBUG=1"])
+    for part in ("step_kernel", "select_kernel", "compact_kernel", "geometry_kernel"):
+        assert "global_atomic_or" in _kernel_body(dbg, part), part

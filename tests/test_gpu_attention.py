@@ -13,13 +13,22 @@ lane group then adds at most a few hundred rows in fp32 (relative error below
 Eviction: the kept set, the compacted K, V and pos and the running sum follow
 the bar of the pass (tests/parity.py): the GPU's kept set is read back from
 the moved pos payload, and may differ from the oracle's only on a near-tie.
+
+FastCAOTE (App. A, Eq. app_fastcaote): the evicted row must be the oracle's
+argmin of s_j = a_j / (1 - a_j) ||v_j - v_bar||, or a row whose oracle score
+lies within the near-tie band of that minimum.  The band follows the error of
+the kernel's fp32 weights: a logit error dz (log2 units, at most 14 * 2^-24
+of sum_c |q'_c k_c| with q' = q * scale * log2(e)) changes a weight by ln 2 *
+dz relative, and the weight sum and the row's own weight enter the score, so
+the band is 4 ln 2 * dz_max + 2e-5 relative to the minimum, plus an absolute
+1e-6 of the largest finite score (weights that underflow fp32 score 0).
 """
 import numpy as np
 import pytest
 import torch
 
 from paper_2609_23314_amd import synth, vd
-from parity import compare_pass, per_unit, to_np, units, values_f64
+from parity import check_layout, compare_pass, per_unit, to_np, units, values_f64
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
@@ -65,8 +74,48 @@ def kept_from_pos(post_pos, n, N):
     return keep
 
 
+def compare_caote(orc, pre_k, pre_v, post_k, post_v, q_units, scale, n_unit, N_unit, keep_gpu,
+                  pre_pos, post_pos, state):
+    """FastCAOTE eviction of a decode step against the oracle (see the module
+    docstring for the band); returns the number of near-tie units."""
+    ties = 0
+    for i in range(pre_v.shape[0]):
+        n, N = int(n_unit[i]), int(N_unit[i])
+        what = f"unit {i} (n={n}, N={N})"
+        if n == 0:
+            continue
+        s_ref = orc.fastcaote_scores(q_units[i], pre_k[i, :n], pre_v[i, :n], scale)
+        keep_ref = orc.select_topn(s_ref, N)
+        kg = np.asarray(keep_gpu[i, :n]).astype(bool)
+        m = min(n, N)
+        if np.array_equal(kg, keep_ref.astype(bool)):
+            ref_k, ref_v, ref_pos = pre_k[i].copy(), pre_v[i].copy(), pre_pos[i].copy()
+            orc.compact(ref_k, ref_v, n, N, keep_ref, ref_pos)
+            assert np.array_equal(post_v[i, :m], ref_v[:m]), f"{what}: V differs"
+            assert np.array_equal(post_k[i, :m], ref_k[:m]), f"{what}: K differs"
+            assert np.array_equal(post_pos[i, :m], ref_pos[:m]), f"{what}: pos differs"
+        else:
+            assert kg.sum() == m, what
+            j_o = int(np.flatnonzero(~keep_ref.astype(bool))[0])
+            j_g = int(np.flatnonzero(~kg)[0])
+            qk = np.abs(q_units[i] * scale * np.log2(np.e)) @ np.abs(values_f64(pre_k[i, :n])).T
+            dz = 14 * 2.0 ** -24 * qk.max()
+            fin = s_ref[np.isfinite(s_ref)]
+            band = (4 * np.log(2) * dz + 2e-5) * s_ref[j_o] + 1e-6 * (fin.max() if fin.size else 0)
+            assert s_ref[j_g] - s_ref[j_o] <= band, (f"{what}: GPU evicted {j_g} (s={s_ref[j_g]!r}), "
+                                                     f"oracle {j_o} (s={s_ref[j_o]!r}), band {band:.3g}")
+            ties += 1
+            for post, pre in ((post_v, pre_v), (post_k, pre_k), (post_pos, pre_pos)):
+                check_layout(post[i], pre[i], kg, n, N, what)
+        want = values_f64(post_v[i, :m]).sum(axis=0)
+        assert state[i, -1] == m, what
+        tol = 1e-12 * np.abs(values_f64(post_v[i, :m])).sum(axis=0) + 1e-300
+        assert np.all(np.abs(state[i, :-1] - want) <= tol), f"{what}: running sum differs"
+    return ties
+
+
 def run_case(orc, S, L, H, G, C, D, dtype, n, N, seed, qscale=1.0, same_rows=False,
-             sample=None, count=None, k_ramp=None):
+             sample=None, count=None, k_ramp=None, variant="l2"):
     k, v = make_cache(S, L, H, C, D, dtype, n, seed, same_rows)
     if k_ramp is not None:
         # every key row is slot 0's row times (1 + k_ramp * slot)
@@ -86,7 +135,7 @@ def run_case(orc, S, L, H, G, C, D, dtype, n, N, seed, qscale=1.0, same_rows=Fal
     g.manual_seed(seed + 7)
     q = torch.randn((S, L, H * G, D), generator=g, device=DEV) * qscale
     scale = D ** -0.5
-    out = vd.vd_decode_attention_evict(k, v, q, n, N, rs, scale=scale, pos=pos)
+    out = vd.vd_decode_attention_evict(k, v, q, n, N, rs, scale=scale, pos=pos, variant=variant)
     torch.cuda.synchronize()
     o = out.cpu().numpy().reshape(U, G, D)
     qn = q.cpu().numpy().astype(np.float64).reshape(U, G, D)
@@ -103,6 +152,12 @@ def run_case(orc, S, L, H, G, C, D, dtype, n, N, seed, qscale=1.0, same_rows=Fal
     post_pos = to_np(pos)[idx]
     keep = np.stack([kept_from_pos(post_pos[i], int(n_u[u]), int(N_u[u]))
                      for i, u in enumerate(idx)])
+    if variant == "fastcaote":
+        ties = compare_caote(orc, pre_k, pre_v, units(to_np(k))[idx], units(to_np(v))[idx],
+                             qn[idx], scale, n_u[idx], N_u[idx], keep,
+                             np.arange(C, dtype=np.int32)[None].repeat(len(idx), 0), post_pos,
+                             to_np(rs)[idx])
+        return ties, k, v, rs, pos
     rep = compare_pass(orc, pre_k, pre_v, units(to_np(k))[idx], units(to_np(v))[idx],
                        n_u[idx], N_u[idx], "l2", dtype, keep_gpu=keep,
                        pre_pos=np.arange(C, dtype=np.int32)[None].repeat(len(idx), 0),
@@ -166,6 +221,63 @@ def test_decode_step_many_sequences(orc):
     N = [max(1, x - (s % 2)) for s, x in enumerate(n)]
     rep, *_ = run_case(orc, 300, 1, 1, 2, 48, 64, torch.bfloat16, n, N, seed=65)
     print(rep)
+
+
+@pytest.mark.parametrize("dt", list(DTYPES))
+@pytest.mark.parametrize("D", [64, 128, 256])
+@pytest.mark.parametrize("G", [1, 2, 4])
+def test_fastcaote_decode_step_matches_oracle(orc, dt, D, G):
+    """FastCAOTE in the fused decode step (App. A, Eq. app_fastcaote): the
+    attention output as for ValueDiff, and the eviction of the row with the
+    lowest a_j / (1 - a_j) ||v_j - v_bar||."""
+    ties, *_ = run_case(orc, 3, 2, 2, G, 320, D, DTYPES[dt], [300, 201, 150], [299, 200, 200],
+                        seed=540 + D + G, variant="fastcaote")
+    assert ties <= 1, ties
+
+
+def test_fastcaote_uniform_attention_evicts_like_valuediff(orc):
+    """Zero queries weigh every row 1/n, so FastCAOTE's scores are the L2
+    scores / (n - 1) and it evicts the row ValueDiff evicts (App. A: the
+    max-entropy limit); identical caches, identical results."""
+    S, L, H, G, C, D = 2, 1, 4, 4, 700, 128
+    n, N = [700, 513], [699, 512]
+    k, v = make_cache(S, L, H, C, D, torch.bfloat16, n, seed=550)
+    U = S * L * H
+    cnt = np.repeat(np.asarray(n) - 1, L * H)
+    outs = []
+    for variant in ("l2", "fastcaote"):
+        kk, vv = k.clone(), v.clone()
+        rs = state_covering(units(to_np(vv)), cnt)
+        pos = torch.arange(C, dtype=torch.int32, device=DEV).repeat(U, 1).contiguous()
+        q = torch.zeros((S, L, H * G, D), device=DEV)
+        vd.vd_decode_attention_evict(kk, vv, q, n, N, rs, pos=pos, variant=variant)
+        torch.cuda.synchronize()
+        outs.append((kk, vv, rs, pos))
+    for a, b in zip(outs[0], outs[1]):   # bit patterns: the tail rows hold NaN
+        assert torch.equal(a.contiguous().view(torch.uint8), b.contiguous().view(torch.uint8))
+
+
+def test_fastcaote_sharp_and_rising_logits(orc):
+    """Nearly one-hot softmax (large queries), and logits that rise along the
+    slots: rows that take almost all the weight score near +infinity, rows
+    whose weight underflows fp32 score 0 (the highest such slot goes)."""
+    # (rows whose weight underflows fp32 in every head tie at 0 on the GPU, so
+    # near-ties are expected here; compare_caote checks each against the band)
+    run_case(orc, 2, 1, 2, 4, 520, 128, torch.bfloat16, [513, 400], [512, 399],
+             seed=563, qscale=30.0, variant="fastcaote")
+    run_case(orc, 16, 1, 8, 4, 1040, 128, torch.bfloat16, [1025] * 16, [1024] * 16,
+             seed=567, qscale=2.0, k_ramp=0.05, variant="fastcaote")
+
+
+def test_fastcaote_decode_workload_layer(orc):
+    """The decode workload's shape, one layer per call (16 x 8 units, 32 query
+    heads, n = 4097, N = 4096, 6 row splits per unit), 12 sampled units."""
+    S, H, G, D, N = 16, 8, 4, 128, 4096
+    rng = np.random.default_rng(571)
+    idx = np.sort(rng.choice(S * H, size=12, replace=False))
+    ties, *_ = run_case(orc, S, 1, H, G, N + 1, D, torch.bfloat16, [N + 1] * S, [N] * S,
+                        seed=572, sample=idx, variant="fastcaote")
+    assert ties <= 1
 
 
 def test_decode_steps_in_a_row(orc):

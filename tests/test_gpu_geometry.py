@@ -42,10 +42,24 @@ def dmax(rows):
     return float(np.sqrt(((x - x.mean(axis=0)) ** 2).sum(axis=1)).max())
 
 
-def check_units(orc, k, v, n_seq, L, H, sample=None):
+def column_sums(x, count_unit):
+    """[U, D + 1]: fp64 column sums of the first count rows of every unit and
+    the count (torch on the GPU: an input of the HIP path, exact for bf16)."""
+    S, L, H, C, D = x.shape
+    xu = x.reshape(S * L * H, C, D)
+    t = torch.zeros((S * L * H, D + 1), dtype=torch.float64, device=DEV)
+    for u in range(S * L * H):
+        c = int(count_unit[u])
+        t[u, :D] = xu[u, :c].double().sum(dim=0)
+        t[u, D] = c
+    return t
+
+
+def check_units(orc, k, v, n_seq, L, H, sample=None, sums=None):
     """Runs vd_geometry on [S, L, H, C, D] caches and compares every unit (or
-    the sampled ones) with the oracle."""
-    out = vd.vd_geometry(k, v, n_seq)
+    the sampled ones) with the oracle; `sums` = (k_sum, v_sum) or None."""
+    kw = {} if sums is None else dict(k_sum=sums[0], v_sum=sums[1])
+    out = vd.vd_geometry(k, v, n_seq, **kw)
     torch.cuda.synchronize()
     got = out.cpu().numpy()
     ku, vu = units(to_np(k)), units(to_np(v))
@@ -84,6 +98,28 @@ def test_geometry_matches_oracle(orc, dt, D):
     n = [1000, 333]
     k, v = make(2, 2, 2, 1024, D, DTYPES[dt], n, seed=300 + D)
     check_units(orc, k, v, n, 2, 2)
+
+
+@pytest.mark.parametrize("dt", list(DTYPES))
+@pytest.mark.parametrize("D", [64, 128, 256])
+def test_geometry_with_column_sums(orc, dt, D):
+    """Column sums of K and V covering exactly the n rows give the centroids
+    up front and one read of the rows; a unit whose sums cover fewer rows
+    (here the second sequence's) takes its centroids from the rows.  Both
+    meet the oracle's bar, and with bf16 rows (exact fp64 sums) the results
+    equal those computed without sums bit for bit."""
+    n = [1000, 333]
+    k, v = make(2, 2, 2, 1024, D, DTYPES[dt], n, seed=310 + D)
+    count = np.repeat([1000, 300], 4)
+    sums = (column_sums(k, count), column_sums(v, count))
+    got = check_units(orc, k, v, n, 2, 2, sums=sums)
+    plain = vd.vd_geometry(k, v, n).cpu().numpy()
+    if dt == "bf16":
+        assert np.array_equal(got, plain)
+    # the one-read path also on a centroid far from the origin
+    k2, v2 = make(1, 1, 2, 800, 128, DTYPES[dt], [777], seed=43, dist="shifted", scale=0.05)
+    c2 = np.repeat([777], 2)
+    check_units(orc, k2, v2, [777], 1, 2, sums=(column_sums(k2, c2), column_sums(v2, c2)))
 
 
 @pytest.mark.parametrize("dt", list(DTYPES))

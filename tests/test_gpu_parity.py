@@ -16,6 +16,8 @@ from parity import (check_scores, compare_pass, per_unit, score_scale, to_np, un
 pytestmark = pytest.mark.gpu
 DEV = "cuda"
 VARIANTS = ["l2", "dir", "norm"]
+KEY_VARIANTS = ["key_l2", "key_dir", "key_norm"]   # the same forms on K; KeyNorm keeps smallest
+ALL_VARIANTS = VARIANTS + KEY_VARIANTS
 DTYPES = {"bf16": torch.bfloat16, "f32": torch.float32}
 
 
@@ -64,7 +66,7 @@ def run_step_case(orc, S, L, H, C, D, dtype, n, N, variant, seed, state="none",
     if state == "zero":
         rs = torch.zeros((U, D + 1), dtype=torch.float64, device=DEV)
     elif state == "incremental":
-        rs = state_for(pre_v, per_unit(count, L, H), D)
+        rs = state_for(pre_k if variant.startswith("key") else pre_v, per_unit(count, L, H), D)
     vd.vd_evict_step(k if k_present else None, v, n, N, variant, running_sum=rs, pos=pos,
                      scores_out=scores, keep_out=keep)
     torch.cuda.synchronize()
@@ -79,7 +81,7 @@ def run_step_case(orc, S, L, H, C, D, dtype, n, N, variant, seed, state="none",
 
 @pytest.mark.parametrize("dt", list(DTYPES))
 @pytest.mark.parametrize("D", [64, 128, 256])
-@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("variant", ALL_VARIANTS)
 def test_score_matches_oracle(orc, dt, D, variant):
     dtype = DTYPES[dt]
     S, L, H, C = 2, 2, 3, 1400
@@ -88,9 +90,9 @@ def test_score_matches_oracle(orc, dt, D, variant):
     U = S * L * H
     scores = torch.full((U, C), -1.0, device=DEV)
     mean = torch.zeros((U, D), device=DEV)
-    vd.vd_score(v, n, variant, scores, mean)
+    vd.vd_score(v, n, variant, scores, mean, k=k)
     torch.cuda.synchronize()
-    pre_v = units(to_np(v))
+    pre_v = units(to_np(k if variant.startswith("key") else v))   # the scored rows
     sg, mg = to_np(scores), to_np(mean)
     nu = per_unit(n, L, H)
     for u in range(U):
@@ -208,7 +210,7 @@ def test_compact_with_unbalanced_masks(orc):
 
 @pytest.mark.parametrize("dt", list(DTYPES))
 @pytest.mark.parametrize("D", [64, 128, 256])
-@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("variant", ALL_VARIANTS)
 def test_step_matches_oracle(orc, dt, D, variant):
     """Prefill boundary, decode step and no-op units in one launch."""
     dtype = DTYPES[dt]
@@ -219,7 +221,7 @@ def test_step_matches_oracle(orc, dt, D, variant):
 
 @pytest.mark.parametrize("dt", list(DTYPES))
 @pytest.mark.parametrize("state", ["zero", "incremental"])
-@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("variant", ALL_VARIANTS)
 def test_step_with_running_sum(orc, dt, state, variant):
     dtype = DTYPES[dt]
     n, N = [1300, 801, 300, 650], [1000, 800, 400, 640]
@@ -229,7 +231,35 @@ def test_step_with_running_sum(orc, dt, state, variant):
     assert rep.near_ties <= 2, rep
 
 
-@pytest.mark.parametrize("dt,D,variant", [("bf16", 128, "l2"), ("f32", 256, "dir"), ("bf16", 64, "norm")])
+@pytest.mark.parametrize("dt,shift", [("f32", 1.0e4), ("f32", -3.0e5), ("bf16", 256.0)])
+@pytest.mark.parametrize("state", ["none", "incremental"])
+def test_l2_far_from_the_origin(orc, dt, shift, state):
+    """L2 scores are invariant under a common shift of the value rows (Sec.
+    3.2, Eq. vd): with every row moved far from the origin the GPU's scores
+    still meet the relative bar with the absolute floor at 1e-6 of the largest
+    score, because the mean is subtracted as a pair of fp32 numbers (an fp32
+    mean alone would be off by 2^-24 * |shift| per channel, about 1e-4 of a
+    score here)."""
+    dtype = DTYPES[dt]
+    S, L, H, C, D = 2, 1, 3, 1200, 128
+    n, N, count = [1200, 1001], [1000, 1000], [1000, 1000]
+    k, v = make_cache(S, L, H, C, D, dtype, n, seed=150)
+    v[:] = (v.float() + shift).to(dtype)   # rows past n stay NaN
+    U = S * L * H
+    pre_k, pre_v = units(to_np(k)), units(to_np(v))
+    rs = None if state == "none" else state_for(pre_v, per_unit(count, L, H), D)
+    scores = torch.full((U, C), -1.0, device=DEV)
+    keep = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
+    vd.vd_evict_step(k, v, n, N, "l2", running_sum=rs, scores_out=scores, keep_out=keep)
+    torch.cuda.synchronize()
+    rep = compare_pass(orc, pre_k, pre_v, units(to_np(k)), units(to_np(v)), per_unit(n, L, H),
+                       per_unit(N, L, H), "l2", dtype, scores_gpu=to_np(scores),
+                       keep_gpu=to_np(keep), state=to_np(rs) if rs is not None else None)
+    assert rep.near_ties <= 2, rep
+
+
+@pytest.mark.parametrize("dt,D,variant", [("bf16", 128, "l2"), ("f32", 256, "dir"), ("bf16", 64, "norm"),
+                                         ("bf16", 128, "key_norm")])
 def test_step_at_maximum_capacity(orc, dt, D, variant):
     """n at the ABI's slot limit (16384): every wave's selection segment is
     full, the keys fill 64 KB of LDS and nothing is staged; one unit evicts a
@@ -243,7 +273,7 @@ def test_step_at_maximum_capacity(orc, dt, D, variant):
 
 @pytest.mark.parametrize("dt", list(DTYPES))
 @pytest.mark.parametrize("state", ["none", "incremental"])
-@pytest.mark.parametrize("variant", VARIANTS)
+@pytest.mark.parametrize("variant", ALL_VARIANTS)
 def test_step_partial_staging(orc, dt, state, variant):
     """Rows to stage (the appended part, or all n rows without a state) that do
     not all fit in LDS at head_dim 256: the first ones are staged and the rest
@@ -324,6 +354,59 @@ def test_step_tiny_units(orc):
     """n = 0, n = 1, N = 1 and n == N in one launch."""
     run_step_case(orc, 5, 1, 1, 8, 64, torch.float32, n=[0, 1, 2, 8, 5], N=[1, 1, 1, 8, 2],
                   variant="l2", seed=95, state="zero")
+
+
+@pytest.mark.parametrize("variant", KEY_VARIANTS)
+def test_key_side_reads_keys_and_moves_values_along(orc, variant):
+    """A key-side pass scores K (V holds rows that would keep another set) and
+    moves V, K and pos together; KeyNorm at n = N + 1 evicts the largest key
+    norm, the highest slot among equal ones."""
+    S, L, H, C, D = 2, 1, 2, 900, 128
+    n, N = [900, 801], [700, 800]
+    k, v = make_cache(S, L, H, C, D, torch.bfloat16, n, seed=160)
+    v[:, :, :, :, 0] = v[:, :, :, :, 0] * 50.0   # value scores would differ wildly
+    k[1, 0, 1, 3] = k[1, 0, 1, 3] * 4.0          # unit 3: the largest key norm at slot 3 ...
+    k[1, 0, 1, 800] = k[1, 0, 1, 3]              # ... and an equal one at the new slot 800
+    U = S * L * H
+    pre_k, pre_v = units(to_np(k)), units(to_np(v))
+    pos = torch.arange(C, dtype=torch.int32, device=DEV).repeat(U, 1).contiguous()
+    scores = torch.zeros((U, C), device=DEV)
+    keep = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
+    vd.vd_evict_step(k, v, n, N, variant, pos=pos, scores_out=scores, keep_out=keep)
+    torch.cuda.synchronize()
+    rep = compare_pass(orc, pre_k, pre_v, units(to_np(k)), units(to_np(v)), per_unit(n, L, H),
+                       per_unit(N, L, H), variant, torch.bfloat16, scores_gpu=to_np(scores),
+                       keep_gpu=to_np(keep), pre_pos=np.tile(np.arange(C, dtype=np.int32), (U, 1)),
+                       post_pos=to_np(pos))
+    assert rep.near_ties == 0, rep
+    if variant == "key_norm":   # unit 3: the highest slot of the two largest norms goes
+        kg = to_np(keep)[3, :801]
+        assert kg[3] == 1 and kg[800] == 0 and kg.sum() == 800
+
+
+def test_key_norm_fused_equals_separate_calls_on_negated_scores(orc):
+    """KeyNorm through the separate calls: vd_score gives the norms, and
+    vd_select_topn on their negatives keeps the smallest (equal norms to the
+    lower slot), so that vd_compact then leaves the fused pass's caches."""
+    S, L, H, C, D = 2, 2, 2, 1100, 64
+    n, N = [1100, 901], [800, 900]
+    k1, v1 = make_cache(S, L, H, C, D, torch.float32, n, seed=170)
+    k1[:, :, :, 5] = k1[:, :, :, 9]   # equal norms
+    k2, v2 = k1.clone(), v1.clone()
+    U = S * L * H
+    s1 = torch.zeros((U, C), device=DEV)
+    kp1 = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
+    vd.vd_evict_step(k1, v1, n, N, "key_norm", scores_out=s1, keep_out=kp1)
+    s2, _ = vd.vd_score(v2, n, "key_norm", k=k2)
+    kp2 = vd.vd_select_topn(v2, (-s2).contiguous(), n, N)
+    vd.vd_compact(k2, v2, kp2, n, N)
+    torch.cuda.synchronize()
+    nu = per_unit(n, L, H)
+    for u in range(U):
+        assert torch.equal(s1[u, :nu[u]], s2[u, :nu[u]])
+        assert torch.equal(kp1[u, :nu[u]], kp2[u, :nu[u]])
+    assert torch.equal(k1.view(torch.int32), k2.view(torch.int32))   # bits: tails hold NaN
+    assert torch.equal(v1.view(torch.int32), v2.view(torch.int32))
 
 
 def test_fused_equals_separate_calls(orc):

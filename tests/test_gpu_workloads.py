@@ -141,11 +141,11 @@ def test_llama_prefill_boundary_all_units(orc, parity_log):
 
 def test_llama_prefill_oracle_forced_boundaries(orc, parity_log):
     """The first three evicting boundaries of the prompt, oracle-forced, with
-    all three variants."""
+    the three value-side and the three key-side scores."""
     w = synth.llama_prefill()
     N, B, D = w.budget[0], w.block, w.head_dim
     U, C = w.units, w.capacity
-    for variant in ("l2", "dir", "norm"):
+    for variant in ("l2", "dir", "norm", "key_l2", "key_dir", "key_norm"):
         ok = np.zeros((U, C, D), np.uint16)
         ov = np.zeros((U, C, D), np.uint16)
         n_o = 0
@@ -160,7 +160,7 @@ def test_llama_prefill_oracle_forced_boundaries(orc, parity_log):
             if n > N:
                 k5 = from_np(ok, w.dtype, DEV).view(1, 32, 8, C, D)
                 v5 = from_np(ov, w.dtype, DEV).view(1, 32, 8, C, D)
-                rs = gpu_state(v5, [n_o], D)
+                rs = gpu_state(k5 if variant.startswith("key") else v5, [n_o], D)
                 sc = torch.zeros((U, C), device=DEV)
                 kp = torch.zeros((U, C), dtype=torch.uint8, device=DEV)
                 vd.vd_evict_step(k5, v5, [n], [N], variant, running_sum=rs, scores_out=sc,
