@@ -29,8 +29,9 @@ Other modes (each prints one JSON line of the same form):
   --geometry             vd_geometry over the workload's cache at capacity
   --decode-attention     the fused decode step (vd_decode_attention_evict)
   --copy-calibration     a plain 1 GiB copy, the reference of the counters
-  --summarize-traces DIR / --summarize-counters DIR   turn rocprofv3 CSV
-                         output into the summaries kept in profiles/
+  --summarize-traces DIR / --summarize-counters DIR / --summarize-sq DIR
+                         turn rocprofv3 CSV output into the summaries kept
+                         in profiles/
 """
 import argparse
 import csv
@@ -559,6 +560,25 @@ def summarize_counters(args):
                       "traffic_over_alg": out["traffic_over_alg"]}))
 
 
+def summarize_sq(args):
+    """Prints, per kernel of --kernels, the mean per dispatch of every counter
+    of one rocprofv3 --pmc run (the directory under --summarize-sq) over its
+    last --last dispatches, as a markdown table."""
+    d = args.summarize_sq
+    rows = _csv_rows(d, "counter_collection")
+    lines = ["| kernel | counter | mean per dispatch |", "|---|---|---|"]
+    for kern in [k.strip() for k in args.kernels.split(",")]:
+        by = {}
+        for r in rows:
+            if kern in r["Kernel_Name"]:
+                by.setdefault(r["Counter_Name"], {}).setdefault(int(r["Dispatch_Id"]), 0.0)
+                by[r["Counter_Name"]][int(r["Dispatch_Id"])] += float(r["Counter_Value"])
+        for name in sorted(by):
+            vals = [by[name][i] for i in sorted(by[name])][-args.last:]
+            lines.append(f"| `{kern}` | {name} | {statistics.mean(vals):.6g} |")
+    print("\n".join(lines))
+
+
 def summarize_traces(args):
     """Prints a markdown summary of one rocprofv3 --kernel-trace --stats run
     (the directory under --summarize-traces, with the bench's JSON line in
@@ -944,6 +964,7 @@ def main():
                          "HBM byte counters) and exit")
     ap.add_argument("--summarize-traces", metavar="DIR")
     ap.add_argument("--summarize-counters", metavar="DIR")
+    ap.add_argument("--summarize-sq", metavar="DIR")
     ap.add_argument("--kernels", default="step_kernel<",
                     help="kernel name substrings for the summaries, comma separated")
     ap.add_argument("--last", type=int, default=60, help="dispatches the summaries average")
@@ -955,6 +976,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(args)
+        return
+    if args.summarize_sq:
+        summarize_sq(args)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the eviction pass has no cross-GPU step "
