@@ -372,9 +372,20 @@ __device__ __forceinline__ uint32_t sum_below16(uint32_t x, int i) {
 // evl starts with the holes below N); keep_out is written if given.  Returns
 // the number of movers.
 // keys_words: 32-bit words of the keys region (the keys, then hist2).
+// Touches (the fused pass): the sweep that gathers the candidates also reads
+// one word of each 128-byte line (at most kTouchLines per row) of the V row of
+// every slot that surely leaves from below N (a hole, whose V row the gather
+// reads for the running sum) and of the K row of every slot that surely moves
+// (tv, tk: the unit's V and K, ss: bytes per slot; null: no touch), so that
+// the gather finds those rows in L2.  The words land in tch, which the caller
+// keeps live until the gather is done (a register reused earlier would make
+// the wave wait for its load); only the sweep's first kTouchIters blocks of 64
+// slots touch.
+constexpr int kTouchIters = 4, kTouchLines = 2;
 __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int N, uint32_t *evl, int evict_cap,
                                                 uint32_t *mvl, int move_cap, uint8_t *keep_out, LdsHead &H,
-                                                int keys_words) {
+                                                int keys_words, const char *tv, const char *tk, uint32_t ss,
+                                                int row_bytes, uint32_t (&tch)[kTouchIters][kTouchLines]) {
     uint32_t *const hist2 = const_cast<uint32_t *>(keys) + ((n + 3) & ~3);
     const int hist2_cap = keys_words - ((n + 3) & ~3);
     const int w = wave_id_s(), lane = lane_id();
@@ -437,13 +448,25 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
         // gather the keys in [lo, hi] and publish this wave's sure evictions
         // (below lo) and sure movers (above hi)
         uint32_t sev = 0u, smv = 0u;
-        for (int jb = j0; jb < j1; jb += 64) {
+        auto sweep = [&](int jb, auto touchc, uint32_t (&t)[kTouchLines]) __attribute__((always_inline)) {
             const int j = jb + lane;
             const bool v = j < j1;
             const uint32_t k = keys[lds_ix<kSiteKeys>(v ? j : j0, n)];
             const bool c = v && k >= lo && k <= hi;
-            sev += __popcll(__ballot(v && k < lo));
-            smv += __popcll(__ballot(v && k > hi && j >= N));
+            const bool gone = v && k < lo, moves = v && k > hi && j >= N;
+            sev += __popcll(__ballot(gone));
+            smv += __popcll(__ballot(moves));
+            if constexpr (decltype(touchc)::value) {
+                const bool hole = gone && j < N;
+                if (hole || (moves && tk)) {
+                    // (a two-way select of the base: a three-way one with a null
+                    // became a table in scratch memory)
+                    const char *row = (hole ? tv : tk) + (uint64_t)j * ss;
+#pragma unroll
+                    for (int l = 0; l < kTouchLines; ++l)
+                        if (l * 128 < row_bytes) t[l] = *reinterpret_cast<const uint32_t *>(row + l * 128);
+                }
+            }
             const uint64_t m = __ballot(c);
             if (m) {
                 uint32_t base = 0u;
@@ -455,7 +478,14 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
                     H.cand_idx[slot] = (uint32_t)j;
                 }
             }
+        };
+        int jb = j0;
+        if (tv) {
+#pragma unroll
+            for (int i = 0; i < kTouchIters; ++i, jb += 64)
+                if (jb < j1) sweep(jb, BoolC<true>{}, tch[i]);
         }
+        for (; jb < j1; jb += 64) sweep(jb, BoolC<false>{}, tch[0]);
         if (lane == 0) {
             H.bc[32 + w] = sev;
             H.bc[48 + w] = smv;
@@ -942,6 +972,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
 
     // ---- select (Sec. 2.1, Eq. eviction) ----
     int n_moves = 0;
+    uint32_t tch[kTouchIters][kTouchLines] = {};  // rows the selection fetched into L2 for the gather
     if (evict) {
         if (amode) {
             // (key << 32) | ~slot: the minimum is the lowest score, highest slot
@@ -975,7 +1006,7 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         } else {
             (void)lds_ix<kSiteKeys>(n - 1, p.keys_cap);  // the keys fit their region
             n_moves = select_and_build(keys, n, N, evl, p.evict_cap, mvl, p.move_cap, keep_out, H,
-                                       keys_words);
+                                       keys_words, vb, p.k ? p.k + off : nullptr, ss32, S::ROWB, tch);
         }
     } else {
         for (int j = threadIdx.x; keep_out && j < n; j += NT) keep_out[j] = 1;
@@ -1118,6 +1149,10 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
                 }
             }
         }
+#pragma unroll
+        for (int i = 0; i < kTouchIters; ++i)
+#pragma unroll
+            for (int l = 0; l < kTouchLines; ++l) asm volatile("" ::"v"(tch[i][l]));
         if (st) {
             const double delta = block_col_total<DT, D>(acc, red, red_cap);  // red aliases keys, no longer needed
             if (threadIdx.x < D) st[threadIdx.x] = (steady ? H.old_sum[threadIdx.x] : H.sum[threadIdx.x]) + delta;
@@ -1161,7 +1196,9 @@ __global__ void __launch_bounds__(NT) select_kernel(const UnitParams p) {
     H.hist[threadIdx.x] = 0u;  // NT == kBins
     if (threadIdx.x == 0) H.bc[100] = 0u;
     __syncthreads();
-    select_and_build(keys, n, N, nullptr, 0, nullptr, 0, keep, H, (p.off_lists - p.off_keys) / 4);
+    uint32_t tch[kTouchIters][kTouchLines];
+    select_and_build(keys, n, N, nullptr, 0, nullptr, 0, keep, H, (p.off_lists - p.off_keys) / 4, nullptr, nullptr,
+                     0u, 0, tch);
 }
 
 // Standalone gather from a keep mask.
