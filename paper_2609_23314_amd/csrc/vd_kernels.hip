@@ -962,6 +962,10 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (threadIdx.x == 0) H.bc[100] = 0u;  // candidate count
     }
     __syncthreads();
+    // Every row load of the stream has been used by now.  Saying so keeps the
+    // compiler from waiting, at a later reuse of a stream register, for loads
+    // it cannot prove complete, which would then include the selection's touches.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     if (scores_out)  // the key holds the score's bits
         for (int j = threadIdx.x; j < n; j += NT) scores_out[j] = score_of<VAR>(keys[lds_ix<kSiteKeys>(j, p.keys_cap)]);
     if (score_mode) {  // the mean leaves after the stream, like the scores
