@@ -374,10 +374,11 @@ __device__ __forceinline__ uint32_t sum_below16(uint32_t x, int i) {
 // keys_words: 32-bit words of the keys region (the keys, then hist2).
 // Touches (the fused pass): the sweep that gathers the candidates also reads
 // one word of each 128-byte line (at most kTouchLines per row) of the V row of
-// every slot that surely leaves from below N (a hole, whose V row the gather
-// reads for the running sum) and of the K row of every slot that surely moves
-// (tv, tk: the unit's V and K, ss: bytes per slot; null: no touch), so that
-// the gather finds those rows in L2.  The words land in tch, which the caller
+// every slot below N that surely leaves or is a candidate (a hole, whose V row
+// the gather reads for the running sum) and of the K row of every slot at or
+// above N that surely stays or is a candidate (a mover) (tv, tk: the unit's V
+// and K, ss: bytes per slot; null: no touch), so that the gather finds those
+// rows in L2.  The words land in tch, which the caller
 // keeps live until the gather is done (a register reused earlier would make
 // the wave wait for its load); only the sweep's first kTouchIters blocks of 64
 // slots touch.
@@ -457,8 +458,9 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
             sev += __popcll(__ballot(gone));
             smv += __popcll(__ballot(moves));
             if constexpr (decltype(touchc)::value) {
-                const bool hole = gone && j < N;
-                if (hole || (moves && tk)) {
+                // (a candidate's row is touched too: half of them leave or move)
+                const bool hole = (gone || c) && j < N;
+                if (hole || ((moves || (c && j >= N)) && tk)) {
                     // (a two-way select of the base: a three-way one with a null
                     // became a table in scratch memory)
                     const char *row = (hole ? tv : tk) + (uint64_t)j * ss;
@@ -884,13 +886,12 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
     // into the same registers as soon as chunk k of t is used: the row loads
     // in flight never drop below one tile less one chunk, and the loads cross
     // from the first part to the second unbroken (the first scoring tile is in
-    // flight while the mean is finished and the staged rows are scored).  The
-    // two parts run as two loops, so that the mean's fp64 partials are dead
-    // while the scoring part runs.
-    auto switch_parts = [&]() __attribute__((always_inline)) {
-        finish_mean();
-        for (int i = 0; i < stash_tiles; ++i) score_stash_tile(i);
-    };
+    // flight while the mean is finished).  The two parts run as two loops, so
+    // that the mean's fp64 partials are dead while the scoring part runs.  The
+    // staged rows are scored from LDS one tile after each scoring tile but the
+    // last, while the next tile's rows are on their way (scored at the switch
+    // they would keep the wave from issuing loads for a while, with one tile
+    // in flight), and any left after the last but one.
     // chunk k of scoring tile tn < tiles (no clamping to other parts needed)
     auto load_scored = [&](int tn, int k, uint32_t z) __attribute__((always_inline)) -> uint4 {
         const int e = (tn - q.tiles_f) * kStep + k * NW * S::RPW + eb;
@@ -947,8 +948,13 @@ __global__ void __launch_bounds__(NT) step_kernel(const UnitParams p) {
         if (q.small) mean_body(eb, eb < fresh, fc);
         for (; t < q.tiles_f && t + 1 < T; ++t) use_fresh(t, std::true_type{});
         if (t < q.tiles_f) use_fresh(t++, std::false_type{});  // no scoring part follows
-        switch_parts();
-        for (; t + 1 < T; ++t) use_scored(t, std::true_type{});
+        finish_mean();
+        int si = 0;  // staged tiles scored
+        for (; t + 1 < T; ++t) {
+            use_scored(t, std::true_type{});
+            if (si < stash_tiles) score_stash_tile(si++);
+        }
+        for (; si < stash_tiles; ++si) score_stash_tile(si);
         if (t < T) use_scored(t, std::false_type{});  // the last tile: no load past the end
     }
     if (to_lds) {  // what the selection reads after the barrier below
