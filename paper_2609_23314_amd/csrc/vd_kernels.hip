@@ -1825,18 +1825,31 @@ __device__ __forceinline__ unsigned long long caote_argmin(const UnitParams &p, 
     }
     const float *rows = p.ws_rows + u * p.capacity * (G + 1);
     unsigned long long best = ~0ull;
-    for (int j = threadIdx.x; j < n; j += kAttnThreads) {
-        float a = 0.f, rest = 0.f;
+    // kRowsAtOnce rows per thread at a time, all their words read before any
+    // is used (one memory round trip per kRowsAtOnce rows, not per row)
+    constexpr int kRowsAtOnce = 4;
+    for (int j0 = threadIdx.x; j0 < n; j0 += kRowsAtOnce * kAttnThreads) {
+        float x[kRowsAtOnce][G + 1];
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-            const float w = __builtin_amdgcn_exp2f(rows[j * (G + 1) + g] - M[g]);
-            a = fmaf(w, inv[g], a);
-            rest = fmaf(fmaxf(Lw[g] - w, 0.f), inv[g], rest);
+        for (int r = 0; r < kRowsAtOnce; ++r) {
+            const int j = min(j0 + r * kAttnThreads, n - 1);  // past the end: row n - 1 again, unused
+#pragma unroll
+            for (int g = 0; g <= G; ++g) x[r][g] = rows[j * (G + 1) + g];
         }
-        const float dist = rows[j * (G + 1) + G];
-        const float sc = rest > 0.f ? (a / rest) * dist : __builtin_inff();  // the 1/G cancels
-        const unsigned long long k = ((unsigned long long)score_key(sc) << 32) | (uint32_t)~(uint32_t)j;
-        best = k < best ? k : best;
+#pragma unroll
+        for (int r = 0; r < kRowsAtOnce; ++r) {
+            const int j = j0 + r * kAttnThreads;
+            float a = 0.f, rest = 0.f;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                const float w = __builtin_amdgcn_exp2f(x[r][g] - M[g]);
+                a = fmaf(w, inv[g], a);
+                rest = fmaf(fmaxf(Lw[g] - w, 0.f), inv[g], rest);
+            }
+            const float sc = rest > 0.f ? (a / rest) * x[r][G] : __builtin_inff();  // the 1/G cancels
+            const unsigned long long k = ((unsigned long long)score_key(sc) << 32) | (uint32_t)~(uint32_t)j;
+            best = j < n && k < best ? k : best;
+        }
     }
     best = wave_min_u64(best);
     if (lane_id() == 0) wbest[wave_id()] = best;
