@@ -808,10 +808,23 @@ def decode_attention_bench(args, dev):
     return res
 
 
-def cpu_decode_attention(w, k, v, q, rs, n, budget_s):
+def _oracle_rate(fn, count, budget_s, threads):
+    """Calls fn(i) for i = 0, 1, ... (cycling over count) on `threads` host
+    threads (ctypes releases the GIL inside the oracle's C) for about budget_s
+    seconds, `threads` calls at a time; returns (calls, seconds)."""
+    from concurrent.futures import ThreadPoolExecutor
+    t0, done = time.perf_counter(), 0
+    with ThreadPoolExecutor(max_workers=threads) as ex:
+        while done == 0 or time.perf_counter() - t0 < budget_s:
+            list(ex.map(fn, [(done + i) % count for i in range(threads)]))
+            done += threads
+    return done, time.perf_counter() - t0
+
+
+def cpu_decode_attention(w, k, v, q, rs, n, budget_s, single_s=3.0):
     """The oracle's attention (every query head) and eviction for units of one
-    layer, one at a time, for about budget_s seconds; scaled to whole steps
-    (all layers) per second."""
+    layer, one unit per call, with every core and with one, scaled to whole
+    steps (all layers) per second."""
     import oracle
     orc = oracle.load()
     S, H, D, C = w.num_seqs, w.num_kv_heads, w.head_dim, w.capacity
@@ -820,36 +833,46 @@ def cpu_decode_attention(w, k, v, q, rs, n, budget_s):
     vn = to_np(v).reshape(S * H, C, D)
     qn = q.cpu().numpy().astype(np.float64).reshape(S * H, G, D)
     m = n[0]
-    t0, done = time.perf_counter(), 0
-    while done < S * H and time.perf_counter() - t0 < budget_s:
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def unit(i):
         for g in range(G):
-            orc.attention(qn[done, g], kn[done, :m], vn[done, :m], D ** -0.5)
-        kc, vc = kn[done:done + 1].copy(), vn[done:done + 1].copy()
-        orc.evict_step(kc, vc, np.array([m], np.int32), np.array([w.budget[0]], np.int32), "l2")
-        done += 1
-    el = time.perf_counter() - t0
-    return {"value": round(done / el / w.units, 4), "unit": "steps/s", "cores": 1,
+            orc.attention(qn[i, g], kn[i, :m], vn[i, :m], D ** -0.5)
+        kc, vc = kn[i:i + 1].copy(), vn[i:i + 1].copy()
+        orc.evict_step(kc, vc, np.array([m], np.int32), np.array([w.budget[0]], np.int32), "l2", nthreads=1)
+
+    d1, e1 = _oracle_rate(unit, S * H, single_s, 1)
+    dn, en = _oracle_rate(unit, S * H, budget_s, threads)
+    what = f"attention of {G} heads and eviction, n={m}"
+    return {"value": round(dn / en / w.units, 4), "unit": "steps/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{done} units of one layer (attention of {G} heads and eviction, n={m}), "
-                      f"one thread, scaled to a step of {w.units} units",
+            "sample": f"{dn} unit calls of one layer ({what}) in {en:.1f} s on {threads} threads, "
+                      f"scaled to a step of {w.units} units",
+            "single_core": {"value": round(d1 / e1 / w.units, 4), "unit": "steps/s", "cores": 1,
+                            "sample": f"{d1} unit calls in {e1:.1f} s, scaled to a step"},
             "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count()}
 
 
-def cpu_geometry(w, k, v, budget_s):
-    """The oracle's geometry of units 0, 1, 2, ... of sequence 0 until about
-    budget_s seconds have passed, scaled to passes over every unit per second."""
+def cpu_geometry(w, k, v, budget_s, single_s=3.0):
+    """The oracle's geometry of the units of sequence 0, one unit per call,
+    with every core and with one, scaled to passes over every unit per second."""
     import oracle
     orc = oracle.load()
     ku = to_np(k[0]).reshape(-1, w.capacity, w.head_dim)
     vu = to_np(v[0]).reshape(-1, w.capacity, w.head_dim)
-    t0, done = time.perf_counter(), 0
-    while done < ku.shape[0] and time.perf_counter() - t0 < budget_s:
-        orc.geometry(ku[done], vu[done])
-        done += 1
-    el = time.perf_counter() - t0
-    return {"value": round(done / el / w.units, 4), "unit": "passes/s", "cores": 1,
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+    def unit(i):
+        orc.geometry(ku[i], vu[i])
+
+    d1, e1 = _oracle_rate(unit, ku.shape[0], single_s, 1)
+    dn, en = _oracle_rate(unit, ku.shape[0], budget_s, threads)
+    return {"value": round(dn / en / w.units, 4), "unit": "passes/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{done} of {w.units} units of {w.capacity} rows, one thread",
+            "sample": f"{dn} unit calls ({w.capacity} rows of K and V each) in {en:.1f} s on "
+                      f"{threads} threads, scaled to passes over all {w.units} units",
+            "single_core": {"value": round(d1 / e1 / w.units, 4), "unit": "passes/s", "cores": 1,
+                            "sample": f"{d1} unit calls in {e1:.1f} s, scaled to whole passes"},
             "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count()}
 
 
