@@ -563,7 +563,8 @@ def summarize_counters(args):
             per.setdefault(str(b), []).append(launches[i])
         out["bytes_per_boundary"] = {b: int(statistics.mean(x)) for b, x in per.items()}
         out["boundaries"] = sorted({int(b) for b in order})
-    alg = bench_line["roofline"]["alg_bytes_per_launch"]
+    # the counters take every launch, the events all but the first of a segment
+    alg = bench_line["roofline"].get("alg_bytes_per_launch_all", bench_line["roofline"]["alg_bytes_per_launch"])
     out["alg_bytes_per_launch"] = alg
     out["traffic_over_alg"] = round(out["bytes_per_launch"] / alg, 4)
     out["dispatches_averaged"] = f"last {K} of each kernel: the timed launches"
@@ -972,7 +973,8 @@ def pass_bench(w, args, dev):
                      "kernel": f"step_kernel<{'bf16' if w.dtype == torch.bfloat16 else 'f32'},"
                                f"{w.head_dim},{variant}>",
                      "launch_us": round(ms_launch * 1e3, 2),
-                     "alg_bytes_per_launch": int(np.mean([alg[i] for i in timed]))},
+                     "alg_bytes_per_launch": int(np.mean([alg[i] for i in timed])),
+                     "alg_bytes_per_launch_all": int(np.mean(alg))},
     }
     if not args.no_cpu_baseline and base_state is not None:
         log("bench: timing the oracle on the host ...")
