@@ -1,7 +1,7 @@
 """Benchmark of the ValueDiff eviction pass on one MI355X.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--variant V]
-                    [--phase prefill|decode] [--no-cpu-baseline]
+                    [--phase prefill|decode] [--no-cpu-baseline] [--launch auto|graph|eager]
 
 A step is one eviction pass (one ``vd_evict_step`` launch: mean, score, top-N,
 gather for every unit) over one boundary of the workload, with its inputs
@@ -14,7 +14,12 @@ evenly over them (boundary floor(i * 60 / K) for pass i), and each timed pass
 consumes a fresh copy of its state, so no pass sees a cache the previous one
 already compacted.  The boundaries timed are printed with the result, and the
 HBM byte counters of profiles/ are kept per boundary, so that the traffic
-reported is the mean over exactly the boundaries timed.
+reported is the mean over exactly the boundaries timed.  The timed passes of
+a segment are launched one by one, or, where a pass moves under 16 MB and
+the host's ~30 us per launch would outlast the kernel (the tiny workload),
+from a captured HIP graph (one host launch per segment); --launch chooses.
+Graph-launched kernels of this size run about 1.5 us apart on this stack, so
+the longer passes are timed from eager launches.
 
 Printed: ONE JSON line with passes/s (value), KV GB/s scanned, the roofline
 of the pass kernel (algorithmic bytes per launch / mean launch time, against
@@ -182,15 +187,20 @@ def scanned_bytes(w, n) -> int:
 
 # ---------------------------------------------------------------- timing
 
-def time_pool(w, states, order, warmup, variant, dev):
+def time_pool(w, states, order, warmup, variant, dev, graph=True):
     """Times one pass per entry of `order` (indices into `states`), each on a
     fresh copy of its pre-pass state.  The copies of a segment are made before
-    it; inside a segment the passes run back to back on one stream.  The wall
-    clock takes every pass; the HIP events take the passes after the first of
-    each segment (the start event is recorded once the first pass is queued,
-    so that the host's latency to the first launch stays out of the per-launch
-    time, which then matches the kernel durations a trace reports).  Returns
-    (wall seconds, GPU milliseconds, the positions in `order` the events took)."""
+    it; inside a segment the passes run back to back on one stream.
+
+    With `graph` the passes of a segment are captured once in a HIP graph and
+    launched by one replay: the host then queues one launch, not one per pass
+    (about 30 us each through Python, which would keep the wall clock above
+    the kernels' time), and the HIP events bracket the replay (the per-launch
+    time carries the replay's one launch latency, spread over the segment).
+    Without it the events start once the first pass is queued and take the
+    rest.  The wall clock takes every pass either way.  Returns (wall seconds,
+    GPU milliseconds, the positions in `order` the events took, "graph" or
+    "eager")."""
     seg_max = len(states)
     work = [(states[0][0].clone(), states[0][1].clone(), states[0][2].clone())
             for _ in range(min(seg_max, len(order)))]
@@ -202,6 +212,22 @@ def time_pool(w, states, order, warmup, variant, dev):
             wv.copy_(states[i][1])
             wr.copy_(states[i][2])
 
+    def passes(idx):
+        for j, i in enumerate(idx):
+            vd.vd_evict_step(work[j][0], work[j][1], states[i][3], w.budget, variant,
+                             running_sum=work[j][2])
+
+    graphs = {}
+
+    def segment_graph(idx):  # (capturing runs nothing: the buffers stay as they are)
+        key = tuple(idx)
+        if key not in graphs:
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                passes(idx)
+            graphs[key] = g
+        return graphs[key]
+
     # The copies above leave up to a few hundred MB of dirty lines in L2 and
     # the MALL; a read of a buffer larger than both evicts them before each
     # timed segment, so that the passes do not pay for the copies' write-back.
@@ -212,28 +238,42 @@ def time_pool(w, states, order, warmup, variant, dev):
         refill([order[i % len(order)]])
         vd.vd_evict_step(work[0][0], work[0][1], st[3], w.budget, variant, running_sum=work[0][2])
     torch.cuda.synchronize()
+    if graph:
+        try:
+            segment_graph(order[:len(work)])
+        except RuntimeError as exc:  # no capture on this stack: time the calls one by one
+            log(f"bench: no HIP graph ({exc}); eager launches")
+            graph = False
     wall_s, gpu_ms, done, timed = 0.0, 0.0, 0, []
     while done < len(order):
         idx = order[done:done + len(work)]
+        g = segment_graph(idx) if graph else None
         refill(idx)
         flush_buf.sum()
         torch.cuda.synchronize()
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
         t0 = time.perf_counter()
-        for j, i in enumerate(idx):
-            vd.vd_evict_step(work[j][0], work[j][1], states[i][3], w.budget, variant,
-                             running_sum=work[j][2])
-            if j == 0:
-                e0.record(stream)
+        if graph:
+            e0.record(stream)
+            g.replay()
+        else:
+            for j, i in enumerate(idx):
+                vd.vd_evict_step(work[j][0], work[j][1], states[i][3], w.budget, variant,
+                                 running_sum=work[j][2])
+                if j == 0:
+                    e0.record(stream)
         e1.record(stream)
         torch.cuda.synchronize()
         wall_s += time.perf_counter() - t0
-        if len(idx) > 1:
+        if graph:
+            gpu_ms += e0.elapsed_time(e1)
+            timed += list(range(done, done + len(idx)))
+        elif len(idx) > 1:
             gpu_ms += e0.elapsed_time(e1)
             timed += list(range(done + 1, done + len(idx)))
         done += len(idx)
-    return wall_s, gpu_ms, timed
+    return wall_s, gpu_ms, timed, "graph" if graph else "eager"
 
 
 def hold(stream):
@@ -894,7 +934,8 @@ def pass_bench(w, args, dev):
         del keep
         log(f"bench: timing {args.steps} decode passes in place")
         total_s, gpu_ms = time_in_place(w, k, v, rs, n, args.steps, args.warmup, variant, dev)
-        timed = list(range(args.steps))
+        timed, launch = list(range(args.steps)), "eager"
+
         alg = [algorithmic_bytes(w, n, movers)] * args.steps
         scan = [scanned_bytes(w, n)] * args.steps
         base_state = (k, v, rs, n, movers, "decode step")
@@ -905,7 +946,7 @@ def pass_bench(w, args, dev):
         total_s, steps, a, sc, (base_state, base_w), head = ragged_prefill(w, variant, args.steps,
                                                                            dev)
         gpu_ms = total_s * 1e3
-        timed = list(range(steps))
+        timed, launch = list(range(steps)), "eager"
         alg, scan = [a / steps] * steps, [sc / steps] * steps
         head_passes = head
     else:
@@ -916,7 +957,10 @@ def pass_bench(w, args, dev):
         order = spread(len(states), args.steps)
         log(f"bench: {len(states)} states ready in {time.perf_counter() - t0:.1f} s; "
             f"timing {args.steps} passes")
-        total_s, gpu_ms, timed = time_pool(w, states, order, args.warmup, variant, dev)
+        small = np.mean([algorithmic_bytes(w, states[i][3], states[i][4]) for i in order]) < 16e6
+        graph = args.launch == "graph" or (args.launch == "auto" and small)
+        total_s, gpu_ms, timed, launch = time_pool(w, states, order, args.warmup, variant, dev,
+                                                   graph=graph)
         alg = [algorithmic_bytes(w, states[i][3], states[i][4]) for i in order]
         scan = [scanned_bytes(w, states[i][3]) for i in order]
         base_state = states[0]
@@ -960,6 +1004,7 @@ def pass_bench(w, args, dev):
                    "prompt": max(w.prompt), "n": max(base_state[3]), "variant": variant,
                    "running_sum": True, "parallelism": "single GPU"},
         "boundaries": order,
+        "launch": launch,
         "head_passes_per_s": round(head_passes / total_s, 1),
         "kv_gbps_scanned": round(scan_gbps, 1),
         "kv_scan_frac_of_hbm_peak": round(scan_gbps / HBM_PEAK_GBPS, 4),
@@ -999,6 +1044,9 @@ def main():
                     help="ragged_serving: the lock-step prefill calls or the decode steps")
     ap.add_argument("--variant", default="l2", choices=sorted(vd.VARIANTS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--launch", default="auto", choices=["auto", "graph", "eager"],
+                    help="how the timed passes are launched: from a captured HIP graph, one by one, "
+                         "or (auto) from a graph only where a pass moves under 16 MB (launch-bound)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--geometry", action="store_true",
                     help="time the geometry diagnostics (vd_geometry) over the workload's "
