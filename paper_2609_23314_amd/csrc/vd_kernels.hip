@@ -125,6 +125,20 @@ __device__ __forceinline__ uint64_t lanes_below() { return (1ull << lane_id()) -
 template <int CTRL> __device__ __forceinline__ float dpp(float x) {
     return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
+// Lane L of each 16-lane row to every lane of that row (row_newbcast).
+template <int L> __device__ __forceinline__ float row_bcast(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x150 + L, 0xF, 0xF, false));
+}
+template <int L> __device__ __forceinline__ long row_bcast(long x) {
+    return __builtin_amdgcn_update_dpp(0L, x, 0x150 + L, 0xF, 0xF, false);
+}
+// f(IntC<0>{}), ..., f(IntC<N-1>{})
+template <int N, int I = 0, typename F> __device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (I < N) {
+        f(IntC<I>{});
+        static_for<N, I + 1>(f);
+    }
+}
 
 // Sum over the LPR lanes holding one row; every lane of the group receives the
 // same bits (each step adds a pair of equal operands in swapped order).
@@ -1642,6 +1656,174 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
     }
     unsigned long long amin = ~0ull;
 
+    // Rows of 16 lanes (bf16 with d = 128, fp32 with d = 64): the tile's
+    // 2 * (G + 1) row sums (G logits and a distance per row) are reduced
+    // together, each exchange leaving every lane with half as many values:
+    // the row's lower half keeps row 0 and its upper half row 1 (row_mirror),
+    // then the even and odd banks of four lanes keep the two heads of a pair
+    // (row_half_mirror), then the quad sums.  Bank k = (lane % 16) / 4 then
+    // holds row k / 2: head k % 2 (and, with G = 4, head 2 + k % 2) and the
+    // distance.  Each bank takes its weights' exponentials once, and every
+    // lane receives all of them by row_newbcast from the first lane of each
+    // bank.
+    constexpr bool kPacked = LPR == 16 && kAttnRows == 2;
+    constexpr int NQ = G == 4 ? 2 : 1;  // logits per lane after the reduction
+    const int bank = (lane & 15) >> 2;
+    const bool upper = bank >= 2, odd = (bank & 1) != 0;
+    const int rb = upper ? 1 : 0;  // this lane's row of the tile after the reduction
+    int hq[NQ];                    // and its heads
+#pragma unroll
+    for (int h = 0; h < NQ; ++h) hq[h] = G == 1 ? 0 : 2 * h + (odd ? 1 : 0);
+    // the references of this lane's heads, and its part of their weight sums
+    // (the weights of row rb only; the row's other half holds the rest)
+    float mxq[NQ], lsq[NQ];
+#pragma unroll
+    for (int h = 0; h < NQ; ++h) {
+        mxq[h] = kNoLogit;
+        lsq[h] = 0.f;
+    }
+    auto packed_tile = [&](int e0, uint4 (&buf)[2 * kAttnRows], auto &&chunk_off, int e_next)
+                           __attribute__((always_inline)) {
+        float a[kAttnRows][G], b[kAttnRows], vx[kAttnRows][EPL];
+        bool valid[kAttnRows];
+#pragma unroll
+        for (int r = 0; r < kAttnRows; ++r) {
+            float kx[EPL];
+            E::unpack(buf[2 * r], kx);
+            E::unpack(buf[2 * r + 1], vx[r]);
+            valid[r] = e0 + r * GROUPS + grp < r1;
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                a[r][g] = 0.f;
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) a[r][g] = fmaf(qs[g][i], kx[i], a[r][g]);
+            }
+            b[r] = 0.f;
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) {
+                const float t = (vx[r][i] - mv[i]) - mvl[i];
+                b[r] = fmaf(t, t, b[r]);
+            }
+            // refill both chunks of this row with the ones of tile e_next
+            const uint32_t zz = zero_after(a[r][0] + b[r]);
+            buf[2 * r] = load_stream(kb, chunk_off(e_next, 2 * r, zz));
+            buf[2 * r + 1] = load_stream(vb, chunk_off(e_next, 2 * r + 1, zz));
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        // row_mirror: the lower half keeps row 0, the upper half row 1
+        float pr[G], pd;
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+            pr[g] = (upper ? a[1][g] : a[0][g]) + dpp<0x140>(upper ? a[0][g] : a[1][g]);
+        pd = (upper ? b[1] : b[0]) + dpp<0x140>(upper ? b[0] : b[1]);
+        // row_half_mirror: even banks keep the pair's first head, odd banks the second
+        float q[NQ];
+        if constexpr (G == 1) {
+            q[0] = pr[0] + dpp<0x141>(pr[0]);
+        } else {
+#pragma unroll
+            for (int h = 0; h < NQ; ++h)
+                q[h] = (odd ? pr[2 * h + 1] : pr[2 * h]) + dpp<0x141>(odd ? pr[2 * h] : pr[2 * h + 1]);
+        }
+        pd += dpp<0x141>(pd);
+#pragma unroll
+        for (int h = 0; h < NQ; ++h) {
+            q[h] += dpp<0x4E>(q[h]);  // quad_perm [2,3,0,1]
+            q[h] += dpp<0xB1>(q[h]);  // quad_perm [1,0,3,2]
+        }
+        pd += dpp<0x4E>(pd);
+        pd += dpp<0xB1>(pd);
+        // this lane's logits: head hq[h] of row rb
+        const bool vr = valid[rb];
+        const int e = e0 + rb * GROUPS + grp;
+        float zq[NQ];
+#pragma unroll
+        for (int h = 0; h < NQ; ++h) zq[h] = vr ? q[h] : kNoLogit;
+        // L2 score of the value row (Sec. 3.2, Eq. vd) and its key
+        const float dist = score_sqrt(pd);
+        if constexpr (CAOTE) {  // the row's logits and distance, for the combine
+            if ((lane & 3) == 0 && vr) {
+#pragma unroll
+                for (int h = 0; h < NQ; ++h)
+                    if (G != 1 || !odd)
+                        rows[lds_ix<kSiteRows>((e - r0) * (G + 1) + hq[h], p.split_rows * (G + 1))] = zq[h];
+                if (!odd) rows[lds_ix<kSiteRows>((e - r0) * (G + 1) + G, p.split_rows * (G + 1))] = dist;
+            }
+        } else {
+            const uint32_t key = score_key(dist);
+            const unsigned long long pk = ((unsigned long long)key << 32) | (uint32_t)~(uint32_t)e;
+            amin = vr && pk < amin ? pk : amin;
+        }
+        // the lazy raise of the references (a wave-uniform branch)
+        bool grow = false;
+#pragma unroll
+        for (int h = 0; h < NQ; ++h) grow = grow || zq[h] > mxq[h] + kLazyLog2;
+        if (__builtin_amdgcn_ballot_w64(grow)) {
+            // every logit of the tile to every lane of its row group
+            float zall[kAttnRows][G];
+            static_for<4>([&](auto kc) __attribute__((always_inline)) {
+                constexpr int k = decltype(kc)::value;
+#pragma unroll
+                for (int h = 0; h < NQ; ++h) {
+                    const float zb = row_bcast<4 * k>(zq[h]);
+                    if (G != 1 || (k & 1) == 0) zall[k >> 1][G == 1 ? 0 : 2 * h + (k & 1)] = zb;
+                }
+            });
+            float cg[G];
+#pragma unroll
+            for (int g = 0; g < G; ++g) {
+                float mn = mx[g];
+#pragma unroll
+                for (int r = 0; r < kAttnRows; ++r) mn = fmaxf(mn, zall[r][g]);
+                cg[g] = __builtin_amdgcn_exp2f(mx[g] - mn);
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) acc[g][i] *= cg[g];
+                mx[g] = mn;
+            }
+#pragma unroll
+            for (int h = 0; h < NQ; ++h) {
+                float c = cg[0], m = mx[0];
+#pragma unroll
+                for (int g = 1; g < G; ++g) {
+                    c = hq[h] == g ? cg[g] : c;
+                    m = hq[h] == g ? mx[g] : m;
+                }
+                lsq[h] *= c;
+                mxq[h] = m;
+            }
+        }
+        // the weights: one exponential per bank and head (an invalid row's
+        // exponent underflows to 0), then to every lane
+        float wq[NQ];
+#pragma unroll
+        for (int h = 0; h < NQ; ++h) {
+            wq[h] = __builtin_amdgcn_exp2f(vr ? zq[h] - mxq[h] : kNoLogit);
+            lsq[h] += wq[h];
+        }
+        float w[kAttnRows][G];
+        static_for<4>([&](auto kc) __attribute__((always_inline)) {
+            constexpr int k = decltype(kc)::value;
+            if constexpr (G == 4) {  // the bank's two weights as one 64-bit move
+                const long pair = ((long)__float_as_int(wq[NQ - 1]) << 32) | (uint32_t)__float_as_int(wq[0]);
+                const long got = row_bcast<4 * k>(pair);
+                w[k >> 1][k & 1] = __int_as_float((int)(uint32_t)got);
+                w[k >> 1][(2 + (k & 1)) % G] = __int_as_float((int)(got >> 32));
+            } else if constexpr (G == 2 || (k & 1) == 0) {
+                w[k >> 1][G == 1 ? 0 : (k & 1) % G] = row_bcast<4 * k>(wq[0]);
+            }
+        });
+#pragma unroll
+        for (int g = 0; g < G; ++g) {
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) {
+                float x = acc[g][i];
+#pragma unroll
+                for (int r = 0; r < kAttnRows; ++r) x = fmaf(w[r][g], vx[r][i], x);
+                acc[g][i] = x;
+            }
+        }
+    };
+
     if (r1 > r0) {
         // chunk j of a tile: row j/2 of this group's kAttnRows rows, K for even j, V for odd
         uint4 buf[2 * kAttnRows];
@@ -1653,7 +1835,12 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
             buf[j] = load_stream((j & 1) ? vb : kb, chunk_off(r0, j, 0u));
             __builtin_amdgcn_sched_barrier(0);
         }
-        for (int e0 = r0; e0 < r1; e0 += A::TILE) {
+        if constexpr (kPacked) {
+            for (int e0 = r0; e0 < r1; e0 += A::TILE) packed_tile(e0, buf, chunk_off, e0 + A::TILE);
+        }
+        for (int e0 = r0; !kPacked && e0 < r1; e0 += A::TILE) {
+          if constexpr (kPacked) {
+          } else {
             float z[kAttnRows][G], vx[kAttnRows][EPL];
             bool valid[kAttnRows];
 #pragma unroll
@@ -1735,7 +1922,15 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 }
                 ls[g] += ws;
             }
+          }
         }
+    }
+    if constexpr (kPacked) {  // head g's weight sum: rows 0 and 1, from banks g % 2 and g % 2 + 2
+        static_for<G>([&](auto gc) __attribute__((always_inline)) {
+            constexpr int g = decltype(gc)::value;
+            constexpr int k0 = G == 1 ? 0 : g % 2;
+            ls[g] = row_bcast<4 * k0>(lsq[g / 2]) + row_bcast<4 * k0 + 8>(lsq[g / 2]);
+        });
     }
 
     // merge the row groups: per head the largest logit, then the rescaled sums
