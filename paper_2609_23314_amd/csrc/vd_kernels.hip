@@ -1682,16 +1682,19 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
         mxq[h] = kNoLogit;
         lsq[h] = 0.f;
     }
-    auto packed_tile = [&](int e0, uint4 (&buf)[2 * kAttnRows], auto &&chunk_off, int e_next)
-                           __attribute__((always_inline)) {
+    // nx[r]: this lane's byte offset in row r of the next tile to load (the
+    // last row of the split stands in past its end)
+    const uint32_t tile_bytes = (uint32_t)A::TILE * ss32, lim_off = row_off(max(r1 - 1, 0), ss32, cl);
+    uint32_t nx[kAttnRows];
+#pragma unroll
+    for (int r = 0; r < kAttnRows; ++r) nx[r] = row_off(r0 + r * GROUPS + grp, ss32, cl) + tile_bytes;
+    auto packed_tile = [&](int e0, uint4 (&buf)[2 * kAttnRows]) __attribute__((always_inline)) {
         float a[kAttnRows][G], b[kAttnRows], vx[kAttnRows][EPL];
-        bool valid[kAttnRows];
 #pragma unroll
         for (int r = 0; r < kAttnRows; ++r) {
             float kx[EPL];
             E::unpack(buf[2 * r], kx);
             E::unpack(buf[2 * r + 1], vx[r]);
-            valid[r] = e0 + r * GROUPS + grp < r1;
 #pragma unroll
             for (int g = 0; g < G; ++g) {
                 a[r][g] = 0.f;
@@ -1704,10 +1707,11 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 const float t = (vx[r][i] - mv[i]) - mvl[i];
                 b[r] = fmaf(t, t, b[r]);
             }
-            // refill both chunks of this row with the ones of tile e_next
-            const uint32_t zz = zero_after(a[r][0] + b[r]);
-            buf[2 * r] = load_stream(kb, chunk_off(e_next, 2 * r, zz));
-            buf[2 * r + 1] = load_stream(vb, chunk_off(e_next, 2 * r + 1, zz));
+            // refill both chunks of this row with the next tile's
+            const uint32_t o = min(nx[r], lim_off) + zero_after(a[r][0] + b[r]);
+            nx[r] += tile_bytes;
+            buf[2 * r] = load_stream(kb, o);
+            buf[2 * r + 1] = load_stream(vb, o);
             __builtin_amdgcn_sched_barrier(0);
         }
         // row_mirror: the lower half keeps row 0, the upper half row 1
@@ -1734,8 +1738,8 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
         pd += dpp<0x4E>(pd);
         pd += dpp<0xB1>(pd);
         // this lane's logits: head hq[h] of row rb
-        const bool vr = valid[rb];
         const int e = e0 + rb * GROUPS + grp;
+        const bool vr = e < r1;
         float zq[NQ];
 #pragma unroll
         for (int h = 0; h < NQ; ++h) zq[h] = vr ? q[h] : kNoLogit;
@@ -1836,7 +1840,7 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
             __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (kPacked) {
-            for (int e0 = r0; e0 < r1; e0 += A::TILE) packed_tile(e0, buf, chunk_off, e0 + A::TILE);
+            for (int e0 = r0; e0 < r1; e0 += A::TILE) packed_tile(e0, buf);
         }
         for (int e0 = r0; !kPacked && e0 < r1; e0 += A::TILE) {
           if constexpr (kPacked) {
