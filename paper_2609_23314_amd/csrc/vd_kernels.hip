@@ -373,7 +373,10 @@ __device__ __forceinline__ uint32_t sum_below16(uint32_t x, int i) {
 // Before the barrier that ended scoring every wave has stored its key minimum
 // in bc[w] and maximum in bc[16 + w], and hist[] and the candidate counter
 // bc[100] are zero; hist2[] (kBins entries, just past the keys) is
-// scratch.  Wave w owns the slot segment [w*seg, (w+1)*seg).
+// scratch.  Wave w owns the slots [j0, j1): a run of whole 64-slot blocks,
+// one more block for the first (blocks mod NW) waves, so that the four waves
+// of each SIMD (w, w+4, w+8, w+12) hold equal shares to within one block (a
+// sweep ends when the busiest SIMD has issued its waves' blocks).
 // Histogram passes over the key range narrow it to one bin (the two histogram
 // buffers alternate, so a pass costs two barriers).  Once the bin holds at
 // most kCand keys, one sweep gathers them and publishes every wave's counts of
@@ -404,9 +407,9 @@ __device__ __forceinline__ int select_and_build(const uint32_t *keys, int n, int
     uint32_t *const hist2 = const_cast<uint32_t *>(keys) + ((n + 3) & ~3);
     const int hist2_cap = keys_words - ((n + 3) & ~3);
     const int w = wave_id_s(), lane = lane_id();
-    const int seg = (((n + NW - 1) / NW) + 63) & ~63;  // slots per wave, whole blocks
-    const int j0 = w * seg;
-    const int j1 = min(n, j0 + seg);
+    const int blocks = (n + 63) >> 6, per = blocks / NW, extra = blocks % NW;
+    const int j0 = 64 * (w * per + min(w, extra));
+    const int j1 = min(n, j0 + 64 * (per + (w < extra ? 1 : 0)));
     uint32_t lo = wave_min_u32(lane < NW ? H.bc[lane] : 0xFFFFFFFFu);
     uint32_t hi = wave_max_u32(lane < NW ? H.bc[16 + lane] : 0u);
     int need = N;       // 1-based rank of (T, J) among the keys in [lo, hi]
