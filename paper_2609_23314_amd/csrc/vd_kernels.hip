@@ -325,19 +325,46 @@ template <int O> __device__ __forceinline__ double xor_sum(double x) {
 // chunk), in a fixed order: thread t < D receives the total of column t (no
 // other thread receives anything).  `red` holds NW*D doubles; the caller
 // orders any later reuse of it with a barrier of its own.
+// One step of a halving sum over the lane pairs (l, l ^ O), O = 16 or 32:
+// the lower lane of each pair keeps p, the upper one q, each summed over the
+// pair with the lower lane's value first (as xor_sum adds).
+template <int O> __device__ __forceinline__ double pair_sum_split(double p, double q) {
+    const unsigned long long bp = __double_as_longlong(p), bq = __double_as_longlong(q);
+    const unsigned plo = (unsigned)bp, phi = (unsigned)(bp >> 32), qlo = (unsigned)bq, qhi = (unsigned)(bq >> 32);
+    const auto L = O == 16 ? __builtin_amdgcn_permlane16_swap(plo, qlo, false, false)
+                           : __builtin_amdgcn_permlane32_swap(plo, qlo, false, false);
+    const auto H = O == 16 ? __builtin_amdgcn_permlane16_swap(phi, qhi, false, false)
+                           : __builtin_amdgcn_permlane32_swap(phi, qhi, false, false);
+    return __longlong_as_double(((unsigned long long)H[0] << 32) | L[0]) +
+           __longlong_as_double(((unsigned long long)H[1] << 32) | L[1]);
+}
 template <int DT, int D>
 __device__ __forceinline__ double block_col_total(double *acc, double *red, int red_cap) {
     using S = Shape<DT, D>;
+    constexpr int E = S::EPL;
+    // The wave's row groups are summed in halving steps (lanes 16 apart, then
+    // 32 apart), each lane keeping half of its columns per step, in the same
+    // association and operand order as summing each column over the row
+    // groups; each lane then writes the totals of the columns it kept.
+    if constexpr (S::LPR <= 8) {
 #pragma unroll
-    for (int i = 0; i < S::EPL; ++i) {
-        if constexpr (S::LPR <= 8) acc[i] = xor_sum<8>(acc[i]);
-        if constexpr (S::LPR <= 16) acc[i] = xor_sum<16>(acc[i]);
-        if constexpr (S::LPR <= 32) acc[i] = xor_sum<32>(acc[i]);
+        for (int i = 0; i < E; ++i) acc[i] = xor_sum<8>(acc[i]);
     }
     const int lane = lane_id(), w = wave_id();
-    if (lane < S::LPR)
+    constexpr int M16 = S::LPR <= 16 ? E / 2 : E;      // columns kept after the step over lanes 16 apart
+    constexpr int M32 = S::LPR <= 32 ? M16 / 2 : M16;  // and after the one over lanes 32 apart
+    static_assert(M32 >= 1, "at least one column per lane");
+    int first = 0;  // the first of this lane's columns within its E
+    double v16[M16], v32[M32];
 #pragma unroll
-        for (int i = 0; i < S::EPL; ++i) red[lds_ix<kSiteRed>(w * D + lane * S::EPL + i, red_cap)] = acc[i];
+    for (int i = 0; i < M16; ++i) v16[i] = S::LPR <= 16 ? pair_sum_split<16>(acc[i], acc[i + M16 % E]) : acc[i];
+    if constexpr (S::LPR <= 16) first += ((lane >> 4) & 1) * M16;
+#pragma unroll
+    for (int i = 0; i < M32; ++i) v32[i] = S::LPR <= 32 ? pair_sum_split<32>(v16[i], v16[(i + M32) % M16]) : v16[i];
+    if constexpr (S::LPR <= 32) first += (lane >> 5) * M32;
+    if (S::LPR > 8 || (lane & 8) == 0)  // lanes 8 apart hold the same totals
+#pragma unroll
+        for (int i = 0; i < M32; ++i) red[lds_ix<kSiteRed>(w * D + (lane % S::LPR) * E + first + i, red_cap)] = v32[i];
     __syncthreads();
     static_assert(D <= NT, "one thread per column");
     double s = 0.0;
