@@ -124,6 +124,28 @@ def test_select_matches_oracle_exactly(orc, ties):
         assert np.all(kg[u, nu[u]:] == 7)
 
 
+@pytest.mark.parametrize("ties", [False, True])
+def test_select_slot_runs(orc, ties):
+    """Slot counts where every wave takes the same number of 64-slot blocks
+    (n = 2048), where all but one take one block more (n = 3000, 47 blocks)
+    and the largest capacity (16384 slots, 16 blocks a wave), with the
+    threshold deep in the order and at its edges."""
+    S, L, H, C, D = 3, 1, 2, 16384, 64
+    n, N = [2048, 3000, 16384], [1500, 2999, 9000]
+    v = torch.zeros((S, L, H, C, D), dtype=torch.float32, device=DEV)
+    U = S * L * H
+    sc = torch.stack([synth.random_scores(C, 300 + u, ties, DEV) for u in range(U)])
+    keep = torch.full((U, C), 7, dtype=torch.uint8, device=DEV)
+    vd.vd_select_topn(v, sc, n, N, keep)
+    torch.cuda.synchronize()
+    kg, s64 = to_np(keep), to_np(sc).astype(np.float64)
+    nu, Nu = per_unit(n, L, H), per_unit(N, L, H)
+    for u in range(U):
+        want = orc.select_topn(s64[u, :nu[u]], int(Nu[u]))
+        assert np.array_equal(kg[u, :nu[u]], want), f"unit {u} (n = {nu[u]})"
+        assert np.all(kg[u, nu[u]:] == 7)
+
+
 def test_select_negative_scores_and_signed_zeros(orc):
     """Scores of any sign (a caller's own ranking), with +0 and -0 mixed: the
     two zeros are one value, so they tie and the lower slot wins."""
