@@ -1872,9 +1872,8 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
         if constexpr (kPacked) {
             for (int e0 = r0; e0 < r1; e0 += A::TILE) packed_tile(e0, buf);
         }
-        for (int e0 = r0; !kPacked && e0 < r1; e0 += A::TILE) {
-          if constexpr (kPacked) {
-          } else {
+        if constexpr (!kPacked) {
+          for (int e0 = r0; e0 < r1; e0 += A::TILE) {
             float z[kAttnRows][G], vx[kAttnRows][EPL];
             bool valid[kAttnRows];
 #pragma unroll
