@@ -21,8 +21,11 @@ LIB = os.path.join(HERE, "libvd.so")
 DEBUG_LIB = os.path.join(HERE, "libvd_debug.so")
 ARCH = "gfx950"
 
-# Packed fp32 instructions are kept out of every device build.
-DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Packed fp32 instructions are kept out of every device build.  MFMA results
+# stay in ordinary VGPRs (the decode split kernel's accumulators would
+# otherwise move to AGPRs and lower its occupancy).
+DEVICE_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+                "-mllvm", "-amdgpu-mfma-vgpr-form"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-Wall", "-I", INCLUDE, "-I", CSRC]
 
 

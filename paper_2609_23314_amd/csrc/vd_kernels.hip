@@ -27,8 +27,10 @@
 //
 // The row stream is software-pipelined: chunk k of tile t+1 is requested as
 // soon as chunk k of tile t is used, and every lane loads unconditionally
-// (rows past the end are clamped to the last row and ignored).  No MFMA:
-// nothing here is a dense contraction.
+// (rows past the end are clamped to the last row and ignored).  The pass
+// has no dense contraction and no MFMA; the fused decode attention's
+// weighted sum of value rows for four query heads per KV head runs on the
+// matrix cores (fp32 4 x 4 x 1 blocks), everything else on the vector ALUs.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -187,7 +189,26 @@ __device__ __forceinline__ uint32_t lane_u32(uint32_t x, int lane) {
 }
 
 // Wave-wide minimum / maximum: DPP inside each 16-lane row, then the four
-// row results by readlane.
+// row results by readlane.  Every lane of the wave takes part.
+template <int CTRL> __device__ __forceinline__ uint64_t dpp_u64(uint64_t x) {
+    return ((uint64_t)dpp_u32<CTRL>((uint32_t)(x >> 32)) << 32) | dpp_u32<CTRL>((uint32_t)x);
+}
+__device__ __forceinline__ uint64_t lane_u64(uint64_t x, int lane) {
+    return ((uint64_t)lane_u32((uint32_t)(x >> 32), lane) << 32) | lane_u32((uint32_t)x, lane);
+}
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
+    uint64_t y = dpp_u64<0xB1>(x);   // quad_perm [1,0,3,2]
+    x = y < x ? y : x;
+    y = dpp_u64<0x4E>(x);            // quad_perm [2,3,0,1]
+    x = y < x ? y : x;
+    y = dpp_u64<0x141>(x);           // row_half_mirror
+    x = y < x ? y : x;
+    y = dpp_u64<0x140>(x);           // row_mirror
+    x = y < x ? y : x;
+    const uint64_t a = lane_u64(x, 0), b = lane_u64(x, 16), c = lane_u64(x, 32), d = lane_u64(x, 48);
+    const uint64_t ab = b < a ? b : a, cd = d < c ? d : c;
+    return cd < ab ? cd : ab;
+}
 __device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) {
     x = min(x, dpp_u32<0xB1>(x));
     x = min(x, dpp_u32<0x4E>(x));
@@ -215,15 +236,9 @@ __device__ __forceinline__ uint32_t wave_incl_scan(uint32_t x) {
     x += dpp_u32<0x143, 0xC>(x);
     return x;
 }
-__device__ __forceinline__ uint64_t wave_min_u64(uint64_t x) {
-    for (int o = 32; o > 0; o >>= 1) {
-        const uint64_t y = __shfl_xor((unsigned long long)x, o);
-        x = y < x ? y : x;
-    }
-    return x;
-}
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // Row addresses are a workgroup-uniform base plus a 32-bit byte offset (the
 // host checks that a unit's slab spans less than 4 GiB), so every access is a
@@ -1698,6 +1713,17 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
     // bank.
     constexpr bool kPacked = LPR == 16 && kAttnRows == 2;
     constexpr int NQ = G == 4 ? 2 : 1;  // logits per lane after the reduction
+    // With G = 4 the weighted sum of the value rows runs on the matrix cores:
+    // v_mfma_f32_4x4x1_16b_f32 treats each quad of lanes as a block whose
+    // 4 x 4 outer product adds (the weight of head i from lane i of the quad)
+    // x (the value of lane j) to row i of lane j.  With lane i of each quad
+    // holding head i's weight and every lane its own value column, accv[k][g]
+    // is acc[g][k]: the same sums, each rounded once per row as the fused
+    // multiply-add chain it replaces.
+    constexpr bool kMfma = kPacked && G == 4;
+    f32x4 accv[EPL];
+#pragma unroll
+    for (int i = 0; i < EPL; ++i) accv[i] = f32x4{0.f, 0.f, 0.f, 0.f};
     const int bank = (lane & 15) >> 2;
     const bool upper = bank >= 2, odd = (bank & 1) != 0;
     const int rb = upper ? 1 : 0;  // this lane's row of the tile after the reduction
@@ -1811,7 +1837,12 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 for (int r = 0; r < kAttnRows; ++r) mn = fmaxf(mn, zall[r][g]);
                 cg[g] = __builtin_amdgcn_exp2f(mx[g] - mn);
 #pragma unroll
-                for (int i = 0; i < EPL; ++i) acc[g][i] *= cg[g];
+                for (int i = 0; i < EPL; ++i) {
+                    if constexpr (kMfma)
+                        accv[i][g] *= cg[g];
+                    else
+                        acc[g][i] *= cg[g];
+                }
                 mx[g] = mn;
             }
 #pragma unroll
@@ -1846,14 +1877,35 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
                 w[k >> 1][G == 1 ? 0 : (k & 1) % G] = row_bcast<4 * k>(wq[0]);
             }
         });
+        if constexpr (kMfma) {
+            // lane i of each quad feeds in head i's weight: head i of row r is
+            // in bank 2r + (i & 1), in the high word of its pair when i >= 2
+            const long pair = ((long)__float_as_int(wq[1]) << 32) | (uint32_t)__float_as_int(wq[0]);
+            const bool odd_head = (lane & 1) != 0, high_head = (lane & 2) != 0;
+            long b0 = row_bcast<0>(pair), b1 = row_bcast<4>(pair), b2 = row_bcast<8>(pair), b3 = row_bcast<12>(pair);
+            // every lane takes part in all four broadcasts (a select between
+            // two broadcasts may otherwise become a branch, each broadcast
+            // then reading lanes the branch has switched off)
+            asm volatile("" : "+v"(b0), "+v"(b1), "+v"(b2), "+v"(b3));
+            const long p0 = odd_head ? b1 : b0;
+            const long p1 = odd_head ? b3 : b2;
+            const float wa[kAttnRows] = {__int_as_float((int)(high_head ? (uint32_t)(p0 >> 32) : (uint32_t)p0)),
+                                         __int_as_float((int)(high_head ? (uint32_t)(p1 >> 32) : (uint32_t)p1))};
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
+            for (int r = 0; r < kAttnRows; ++r)
 #pragma unroll
-            for (int i = 0; i < EPL; ++i) {
-                float x = acc[g][i];
+                for (int i = 0; i < EPL; ++i)
+                    accv[i] = __builtin_amdgcn_mfma_f32_4x4x1f32(wa[r], vx[r][i], accv[i], 0, 0, 0);
+        } else {
 #pragma unroll
-                for (int r = 0; r < kAttnRows; ++r) x = fmaf(w[r][g], vx[r][i], x);
-                acc[g][i] = x;
+            for (int g = 0; g < G; ++g) {
+#pragma unroll
+                for (int i = 0; i < EPL; ++i) {
+                    float x = acc[g][i];
+#pragma unroll
+                    for (int r = 0; r < kAttnRows; ++r) x = fmaf(w[r][g], vx[r][i], x);
+                    acc[g][i] = x;
+                }
             }
         }
     };
@@ -1958,6 +2010,11 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
           }
         }
     }
+    if constexpr (kMfma)
+#pragma unroll
+        for (int g = 0; g < G; ++g)
+#pragma unroll
+            for (int i = 0; i < EPL; ++i) acc[g][i] = accv[i][g];
     if constexpr (kPacked) {  // head g's weight sum: rows 0 and 1, from banks g % 2 and g % 2 + 2
         static_for<G>([&](auto gc) __attribute__((always_inline)) {
             constexpr int g = decltype(gc)::value;
@@ -2017,12 +2074,13 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
 // slot below N (slot reuse) and updates the running sum.  Launched after the
 // split kernel, so every row has been read before anything moves.
 //
-// The eviction is the work of the first LPR threads, thread c owning the
-// columns of chunk c of a row: it loads the argmin words, its state columns
-// and its chunk of the newest row (row N when evicting) all at once, and only
-// the chunk of the evicted row waits for the argmin.  Each thread reads that
-// chunk before it overwrites it, so no barrier is needed; the other threads
-// merge the outputs meanwhile.
+// The eviction is the work of LPR lanes of the last wave, lane c owning the
+// columns of chunk c of a row: they load the argmin words, their state columns
+// and their chunk of the newest row (row N when evicting) all at once; only
+// the chunk of the evicted row waits for the argmin, and its load goes out
+// with the wave's loads of the split partials, so that the wave waits for
+// memory twice and the other waves once.  Each lane reads its chunk of the
+// evicted row before it overwrites it, so no barrier is needed.
 // FastCAOTE scores of a unit's rows (App. A, Eq. app_fastcaote) from the
 // logits and distances its splits stored, and their minimum as (key << 32 |
 // ~slot), the lowest score and the highest slot among equal ones: a_j = (1/G)
@@ -2111,20 +2169,78 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     if constexpr (CAOTE) {
         if (evict) caote_min = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
     }
-    if (threadIdx.x < LPR) {
-        const int c = threadIdx.x;
-        // everything that does not depend on the evicted slot
-        unsigned long long m = caote_min;
-        if constexpr (!CAOTE)
-            for (int s = 0; s < S; ++s) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
-        const double cnt = st[D];
-        double old[EPL];
+    // The eviction lanes: the first LPR lanes of the last wave, lane c owning
+    // chunk c of a row.  Every lane loads (the others chunk 0, so that no
+    // loaded value leaves a branch): first what does not depend on the evicted
+    // slot, then the argmin words of the splits, whose minimum each wave takes;
+    // the evicted row's chunk then goes out with the output loads below.
+    constexpr int kEvWave = kAttnWaves - 1;
+    static_assert(LPR <= 64, "the chunks of a row fit one wave");
+    const int c = threadIdx.x - kEvWave * 64;
+    const bool ev = c >= 0 && c < LPR;
+    const int ce = ev ? c : 0;
+    const int last = n > 0 ? n - 1 : 0;
+    const double cnt = st[D];
+    double old[EPL];
 #pragma unroll
-        for (int i = 0; i < EPL; ++i) old[i] = st[c * EPL + i];
-        const int last = n > 0 ? n - 1 : 0;
-        const uint4 kl = load_stream(kb, row_off(last, ss32, c));
-        const uint4 vl = load_stream(vb, row_off(last, ss32, c));
-        const int32_t pl = (p.pos && evict && c == 0) ? p.pos[u * p.capacity + N] : 0;
+    for (int i = 0; i < EPL; ++i) old[i] = st[ce * EPL + i];
+    const uint4 kl = load_stream(kb, row_off(last, ss32, ce));
+    const uint4 vl = load_stream(vb, row_off(last, ss32, ce));
+    // row N's position (any readable word when there is none to move), by a
+    // vector load (the index in VGPRs), so that no wait for it comes early
+    const bool has_pos = p.pos && evict;
+    const int32_t *pbase = has_pos ? p.pos : reinterpret_cast<const int32_t *>(kb);
+    int64_t pix = has_pos ? u * p.capacity + N : 0;
+    asm volatile("" : "+v"(pix));
+    const int32_t pl = pbase[pix];
+    unsigned long long m = caote_min;
+    if constexpr (!CAOTE) {
+        for (int s = lane_id(); s < S; s += 64) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
+        m = wave_min_u64(m);
+    }
+    const int j = evict ? (int)~(uint32_t)m : -1;
+    const uint4 xj = load_stream(vb, row_off(j >= 0 ? j : 0, ss32, ce));  // used after the outputs
+    // outputs: the splits in batches of kMergeBatch whose loads all go out
+    // together (a split past S reads split s0 again and weighs 0), each batch
+    // raising the running reference to its largest logit
+    float *orow = p.attn_out + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
+    const float *ml = p.ws_ml + u * S * G * 2;
+    const float *pa = p.ws_acc + u * S * G * D;
+#pragma unroll
+    for (int o = 0; o < kOut; ++o) {
+        const int idx = threadIdx.x + o * kAttnThreads;
+        if (idx < G * D) {
+            const int g = idx / D, cc = idx % D;
+            float top = kNoLogit, num = 0.f, den = 0.f;
+            for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
+                float m[kMergeBatch], l[kMergeBatch], a[kMergeBatch];
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) {
+                    const int s = s0 + i < S ? s0 + i : s0;
+                    m[i] = ml[(s * G + g) * 2];
+                    l[i] = ml[(s * G + g) * 2 + 1];
+                    a[i] = pa[(s * G + g) * D + cc];
+                }
+                float bt = top;
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) bt = fmaxf(bt, m[i]);
+                if (s0 > 0) {  // the earlier batches' sums to the new reference
+                    const float r = __builtin_amdgcn_exp2f(top - bt);
+                    num *= r;
+                    den *= r;
+                }
+                top = bt;
+#pragma unroll
+                for (int i = 0; i < kMergeBatch; ++i) {
+                    const float f = s0 + i < S ? __builtin_amdgcn_exp2f(m[i] - top) : 0.f;
+                    num = fmaf(a[i], f, num);
+                    den = fmaf(l[i], f, den);
+                }
+            }
+            orow[g * D + cc] = n > 0 ? num / den : 0.f;
+        }
+    }
+    if (ev) {
         const int count = (cnt >= 0.0 && cnt <= (double)n && cnt == (double)(int)cnt) ? (int)cnt : 0;
         // the rows the state does not cover, in slot order (the newest one is loaded)
         double f[EPL];
@@ -2139,11 +2255,11 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
         double part[EPL];
 #pragma unroll
         for (int i = 0; i < EPL; ++i) part[i] = (count > 0 ? old[i] : 0.0) + f[i];
-        // the evicted row leaves the running sum, read before the move below
-        const int j = evict ? (int)~(uint32_t)m : -1;
+        // the evicted row leaves the running sum; lane c read its chunk before
+        // the move below overwrites it
         if (j >= 0) {
             float x[EPL];
-            E::unpack(load_stream(vb, row_off(j, ss32, c)), x);
+            E::unpack(xj, x);
 #pragma unroll
             for (int i = 0; i < EPL; ++i) part[i] -= (double)x[i];
         }
@@ -2154,48 +2270,6 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
             store_stream(kb, row_off(j, ss32, c), kl);
             store_stream(vb, row_off(j, ss32, c), vl);
             if (p.pos && c == 0) p.pos[u * p.capacity + j] = pl;
-        }
-    }
-    // outputs
-    float *orow = p.attn_out + (((int64_t)sl * p.num_layers + layer) * p.num_kv_heads + head) * G * D;
-    const float *ml = p.ws_ml + u * S * G * 2;
-    const float *pa = p.ws_acc + u * S * G * D;
-#pragma unroll
-    for (int o = 0; o < kOut; ++o) {
-        const int idx = threadIdx.x + o * kAttnThreads;
-        if (idx < G * D) {
-            const int g = idx / D, c = idx % D;
-            // splits in batches of kMergeBatch whose loads all go out together
-            // (a split past S reads split s0 again and weighs 0)
-            float top = kNoLogit;
-            for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
-                float m[kMergeBatch];
-#pragma unroll
-                for (int i = 0; i < kMergeBatch; ++i) {
-                    const int s = s0 + i < S ? s0 + i : s0;
-                    m[i] = ml[(s * G + g) * 2];
-                }
-#pragma unroll
-                for (int i = 0; i < kMergeBatch; ++i) top = fmaxf(top, m[i]);
-            }
-            float num = 0.f, den = 0.f;
-            for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
-                float m[kMergeBatch], l[kMergeBatch], a[kMergeBatch];
-#pragma unroll
-                for (int i = 0; i < kMergeBatch; ++i) {
-                    const int s = s0 + i < S ? s0 + i : s0;
-                    m[i] = ml[(s * G + g) * 2];
-                    l[i] = ml[(s * G + g) * 2 + 1];
-                    a[i] = pa[(s * G + g) * D + c];
-                }
-#pragma unroll
-                for (int i = 0; i < kMergeBatch; ++i) {
-                    const float f = s0 + i < S ? __builtin_amdgcn_exp2f(m[i] - top) : 0.f;
-                    num = fmaf(a[i], f, num);
-                    den = fmaf(l[i], f, den);
-                }
-            }
-            orow[g * D + c] = n > 0 ? num / den : 0.f;
         }
     }
 }
