@@ -306,6 +306,31 @@ def stream_read_gbps(dev, nbytes=2 << 30, reps=5):
     return nbytes / best / 1e9
 
 
+def stream_read_us(dev, nbytes, reps=8):
+    """Time per read of the plain streaming read (vd_stream_read) of `nbytes`:
+    the read ceiling at a kernel's own size, where ramp-up and drain weigh more
+    than at 2 GiB.  `reps` distinct buffers, pushed out of the caches by 256 MiB
+    of writes, are read back to back; the events take all but the first read,
+    so that no launch latency enters (as for the kernels' own per-launch
+    times).  In microseconds."""
+    n = max((nbytes + 15) // 16, 1) * 4  # whole 16-byte words
+    bufs = [torch.ones(n, dtype=torch.float32, device=dev) for _ in range(reps + 1)]
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    flush = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
+    flush.fill_(1)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    vd.vd_stream_read(bufs[0], sink)
+    e0.record()
+    for b in bufs[1:]:
+        vd.vd_stream_read(b, sink)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del bufs, flush
+    return us
+
+
 def decode_state(w: synth.Workload, dev, variant="l2"):
     """A decode step of every sequence: N old tokens and one new token in the
     cache (n = N + 1), and the running sum of the N old rows of the scored
@@ -822,6 +847,7 @@ def decode_attention_bench(args, dev):
     log(f"bench: {us_call:.2f} us per layer call, {gbps:.0f} GB/s algorithmic, {movers} movers of {units}")
     # the eviction pass alone over all layers (vd_evict_step), for context
     _, ev_ms = time_in_place(w, k, v, rs, n, 10, 2, "l2", dev)
+    same_us = stream_read_us(dev, alg)
     res = {
         "metric": "decode steps/s (attention of the newest token fused to its eviction, all layers)",
         "value": round(args.steps / wall, 2),
@@ -841,6 +867,8 @@ def decode_attention_bench(args, dev):
                      "kernel": "attn_split_kernel<bf16,128,4> + attn_combine_kernel (one call)",
                      "launch_us": round(us_call, 2), "alg_bytes_per_launch": alg},
         "evict_pass_alone_us": round(ev_ms * 1e3 / 10, 2),
+        "stream_read_same_bytes_us": round(same_us, 2),
+        "call_over_stream_read_same_bytes": round(us_call / same_us, 3),
     }
     if not args.no_cpu_baseline:
         log("bench: timing the oracle on the host ...")
@@ -979,6 +1007,8 @@ def pass_bench(w, args, dev):
         "_prefill" if args.phase == "prefill" and w.name == "ragged_serving" else "")
     traffic = load_traffic(tname, order)
     stream_gbps = stream_read_gbps(dev)
+    alg_launch = sum(alg[i] for i in timed) / len(timed)
+    same_us = stream_read_us(dev, int(alg_launch))
     out = {
         "metric": METRIC,
         "value": round(passes_per_s, 2),
@@ -1010,6 +1040,8 @@ def pass_bench(w, args, dev):
         "kv_scan_frac_of_hbm_peak": round(scan_gbps / HBM_PEAK_GBPS, 4),
         "stream_read_gbps": round(stream_gbps, 1),
         "alg_frac_of_stream_read": round(alg_gbps / stream_gbps, 4),
+        "stream_read_same_bytes_us": round(same_us, 2),
+        "launch_over_stream_read_same_bytes": round(ms_launch * 1e3 / same_us, 3),
         "roofline": {"bound": "hbm", "achieved": round(alg_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(alg_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": None if traffic is None else int(traffic),
