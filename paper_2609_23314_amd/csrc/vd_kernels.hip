@@ -2068,19 +2068,6 @@ __global__ void __launch_bounds__(kAttnThreads) attn_split_kernel(const UnitPara
     }
 }
 
-// Merges a unit's splits into the attention output of its G query rows, then
-// evicts (n = N + 1: the row with the lowest score, the highest slot among
-// equal lowest scores; Sec. 2.1, Eq. eviction), moves row N into the freed
-// slot below N (slot reuse) and updates the running sum.  Launched after the
-// split kernel, so every row has been read before anything moves.
-//
-// The eviction is the work of LPR lanes of the last wave, lane c owning the
-// columns of chunk c of a row: they load the argmin words, their state columns
-// and their chunk of the newest row (row N when evicting) all at once; only
-// the chunk of the evicted row waits for the argmin, and its load goes out
-// with the wave's loads of the split partials, so that the wave waits for
-// memory twice and the other waves once.  Each lane reads its chunk of the
-// evicted row before it overwrites it, so no barrier is needed.
 // FastCAOTE scores of a unit's rows (App. A, Eq. app_fastcaote) from the
 // logits and distances its splits stored, and their minimum as (key << 32 |
 // ~slot), the lowest score and the highest slot among equal ones: a_j = (1/G)
@@ -2093,11 +2080,44 @@ __device__ __forceinline__ unsigned long long caote_argmin(const UnitParams &p, 
                                                            const float *ml, int S) {
     __shared__ float mg[G], lg[G];
     __shared__ unsigned long long wbest[kAttnWaves];
+    // kRowsAtOnce rows per thread at a time, all their words read before any
+    // is used (one memory round trip per batch; n = 4097 is one batch), the
+    // first batch before the heads' maxima and sums are merged
+    constexpr int kRowsAtOnce = 17;
+    const float *rows = p.ws_rows + u * p.capacity * (G + 1);
+    float x[kRowsAtOnce][G + 1];
+    auto load_rows = [&](int j0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int r = 0; r < kRowsAtOnce; ++r) {
+            const int j = min(j0 + r * kAttnThreads, n - 1);  // past the end: row n - 1 again, unused
+#pragma unroll
+            for (int g = 0; g <= G; ++g) x[r][g] = rows[j * (G + 1) + g];
+        }
+    };
+    load_rows(threadIdx.x);
     if (threadIdx.x < G) {
+        // the splits in batches of kMergeBatch whose loads all go out together
+        // (a split past S reads split s0 again and weighs 0), each batch
+        // raising the running reference to its largest logit
         const int g = threadIdx.x;
         float top = kNoLogit, den = 0.f;
-        for (int s = 0; s < S; ++s) top = fmaxf(top, ml[(s * G + g) * 2]);
-        for (int s = 0; s < S; ++s) den += ml[(s * G + g) * 2 + 1] * __builtin_amdgcn_exp2f(ml[(s * G + g) * 2] - top);
+        for (int s0 = 0; s0 < S; s0 += kMergeBatch) {
+            float m[kMergeBatch], l[kMergeBatch];
+#pragma unroll
+            for (int i = 0; i < kMergeBatch; ++i) {
+                const int s = s0 + i < S ? s0 + i : s0;
+                m[i] = ml[(s * G + g) * 2];
+                l[i] = ml[(s * G + g) * 2 + 1];
+            }
+            float bt = top;
+#pragma unroll
+            for (int i = 0; i < kMergeBatch; ++i) bt = fmaxf(bt, m[i]);
+            if (s0 > 0) den *= __builtin_amdgcn_exp2f(top - bt);
+            top = bt;
+#pragma unroll
+            for (int i = 0; i < kMergeBatch; ++i)
+                if (s0 + i < S) den += l[i] * __builtin_amdgcn_exp2f(m[i] - top);
+        }
         mg[threadIdx.x] = top;
         lg[threadIdx.x] = den;
     }
@@ -2109,19 +2129,9 @@ __device__ __forceinline__ unsigned long long caote_argmin(const UnitParams &p, 
         Lw[g] = lg[g];
         inv[g] = 1.f / Lw[g];
     }
-    const float *rows = p.ws_rows + u * p.capacity * (G + 1);
     unsigned long long best = ~0ull;
-    // kRowsAtOnce rows per thread at a time, all their words read before any
-    // is used (one memory round trip per kRowsAtOnce rows, not per row)
-    constexpr int kRowsAtOnce = 4;
     for (int j0 = threadIdx.x; j0 < n; j0 += kRowsAtOnce * kAttnThreads) {
-        float x[kRowsAtOnce][G + 1];
-#pragma unroll
-        for (int r = 0; r < kRowsAtOnce; ++r) {
-            const int j = min(j0 + r * kAttnThreads, n - 1);  // past the end: row n - 1 again, unused
-#pragma unroll
-            for (int g = 0; g <= G; ++g) x[r][g] = rows[j * (G + 1) + g];
-        }
+        if (j0 != (int)threadIdx.x) load_rows(j0);
 #pragma unroll
         for (int r = 0; r < kRowsAtOnce; ++r) {
             const int j = j0 + r * kAttnThreads;
@@ -2146,6 +2156,20 @@ __device__ __forceinline__ unsigned long long caote_argmin(const UnitParams &p, 
     return m;
 }
 
+// Merges a unit's splits into the attention output of its G query rows, then
+// evicts (n = N + 1: the row with the lowest score, the highest slot among
+// equal lowest scores; Sec. 2.1, Eq. eviction), moves row N into the freed
+// slot below N (slot reuse) and updates the running sum.  Launched after the
+// split kernel, so every row has been read before anything moves.
+//
+// The eviction is the work of LPR lanes of the last wave, lane c owning the
+// columns of chunk c of a row.  Every lane of the block loads its state
+// columns, its chunk of the newest row (row N when evicting) and the argmin
+// words at once (lanes outside the eviction read chunk 0); only the evicted
+// row's chunk waits for the argmin, and it goes out with the loads of the
+// split partials, so that the block waits for memory twice.  Each lane reads
+// its chunk of the evicted row before it overwrites it, so no barrier is
+// needed.
 template <int DT, int D, int G, bool CAOTE>
 __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitParams p) {
     using A = AttnShape<DT, D>;
@@ -2165,15 +2189,13 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     double *st = p.running_sum + u * (D + 1);
     const int S = p.splits;
     const bool evict = n > N;  // the host admits n <= N + 1 only
-    unsigned long long caote_min = ~0ull;
-    if constexpr (CAOTE) {
-        if (evict) caote_min = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
-    }
     // The eviction lanes: the first LPR lanes of the last wave, lane c owning
     // chunk c of a row.  Every lane loads (the others chunk 0, so that no
     // loaded value leaves a branch): first what does not depend on the evicted
-    // slot, then the argmin words of the splits, whose minimum each wave takes;
-    // the evicted row's chunk then goes out with the output loads below.
+    // slot, then the lowest (key, ~slot), from the splits' argmin words (one
+    // per lane, the minimum taken by each wave) or, for FastCAOTE, from every
+    // row's score; the evicted row's chunk then goes out with the output
+    // loads below.
     constexpr int kEvWave = kAttnWaves - 1;
     static_assert(LPR <= 64, "the chunks of a row fit one wave");
     const int c = threadIdx.x - kEvWave * 64;
@@ -2193,8 +2215,10 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     int64_t pix = has_pos ? u * p.capacity + N : 0;
     asm volatile("" : "+v"(pix));
     const int32_t pl = pbase[pix];
-    unsigned long long m = caote_min;
-    if constexpr (!CAOTE) {
+    unsigned long long m = ~0ull;
+    if constexpr (CAOTE) {
+        if (evict) m = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
+    } else {
         for (int s = lane_id(); s < S; s += 64) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
         m = wave_min_u64(m);
     }
