@@ -309,12 +309,14 @@ def stream_read_gbps(dev, nbytes=2 << 30, reps=5):
 def stream_read_us(dev, nbytes, reps=8):
     """Time per read of the plain streaming read (vd_stream_read) of `nbytes`:
     the read ceiling at a kernel's own size, where ramp-up and drain weigh more
-    than at 2 GiB.  `reps` distinct buffers, pushed out of the caches by 256 MiB
-    of writes, are read back to back; the events take all but the first read,
-    so that no launch latency enters (as for the kernels' own per-launch
-    times).  In microseconds."""
+    than at 2 GiB.  `reps` distinct buffers (one, read again, above 512 MiB),
+    pushed out of the caches by 256 MiB of writes, are read back to back; the
+    events take all but the first read, so that no launch latency enters (as
+    for the kernels' own per-launch times).  In microseconds."""
     n = max((nbytes + 15) // 16, 1) * 4  # whole 16-byte words
-    bufs = [torch.ones(n, dtype=torch.float32, device=dev) for _ in range(reps + 1)]
+    # above 512 MiB one buffer, read again and again, outgrows the caches by itself
+    nbuf = reps + 1 if nbytes <= (512 << 20) else 1
+    bufs = [torch.ones(n, dtype=torch.float32, device=dev) for _ in range(nbuf)]
     sink = torch.zeros(1, dtype=torch.int32, device=dev)
     flush = torch.empty(256 << 20, dtype=torch.uint8, device=dev)
     flush.fill_(1)
@@ -322,8 +324,8 @@ def stream_read_us(dev, nbytes, reps=8):
     e1 = torch.cuda.Event(enable_timing=True)
     vd.vd_stream_read(bufs[0], sink)
     e0.record()
-    for b in bufs[1:]:
-        vd.vd_stream_read(b, sink)
+    for i in range(reps):
+        vd.vd_stream_read(bufs[(i + 1) % nbuf], sink)
     e1.record()
     torch.cuda.synchronize()
     us = e0.elapsed_time(e1) * 1e3 / reps
