@@ -84,3 +84,22 @@ def test_lds_checks_only_in_the_debug_build(kernels, tmp_path_factory):
     dbg = _assembly(tmp_path_factory, ["-DVD_DEBUG=1"])
     for part in ("step_kernel", "select_kernel", "compact_kernel", "geometry_kernel"):
         assert "global_atomic_or" in _kernel_body(dbg, part), part
+
+
+def test_decode_split_keeps_three_workgroups_per_cu(kernels):
+    """The host sizes the fused decode step's split launch for three 256-thread
+    workgroups per CU (three waves per SIMD), which holds while each split
+    kernel needs at most 168 registers per lane, AGPRs included (512 per SIMD
+    lane over three waves, in steps of 8).  With four query heads per KV head
+    and 16-lane rows the value sums run on the matrix cores, their
+    accumulators in ordinary VGPRs."""
+    text, bodies, _ = kernels
+    regs = dict(re.findall(r"\.amdhsa_kernel (\S*attn_split_kernel\S*)\n(?:.*\n)*?"
+                           r"\s*\.amdhsa_next_free_vgpr (\d+)", text))
+    assert len(regs) >= 9, regs
+    over = {k: int(v) for k, v in regs.items() if int(v) > 168}
+    assert not over, over
+    for part in ("attn_split_kernelILi0ELi128ELi4E", "attn_split_kernelILi1ELi64ELi4E"):
+        body = _kernel_body(text, part)
+        assert "v_mfma_f32_4x4x1_16b_f32" in body, part
+        assert "v_accvgpr" not in body, part
