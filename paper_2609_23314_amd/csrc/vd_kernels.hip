@@ -2176,7 +2176,6 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     using E = Elem<DT>;
     constexpr int EPL = A::EPL, LPR = A::LPR;
     constexpr int kOut = (G * D + kAttnThreads - 1) / kAttnThreads;  // outputs per thread
-    static_assert(LPR <= kAttnThreads, "one thread per chunk of a row");
     const int head = blockIdx.x;
     const int sl = blockIdx.y / p.num_layers, layer = blockIdx.y % p.num_layers;
     const int ul = (sl * p.num_layers + layer) * p.num_kv_heads + head;
@@ -2215,14 +2214,14 @@ __global__ void __launch_bounds__(kAttnThreads) attn_combine_kernel(const UnitPa
     int64_t pix = has_pos ? u * p.capacity + N : 0;
     asm volatile("" : "+v"(pix));
     const int32_t pl = pbase[pix];
-    unsigned long long m = ~0ull;
+    unsigned long long lowest = ~0ull;
     if constexpr (CAOTE) {
-        if (evict) m = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
+        if (evict) lowest = caote_argmin<G>(p, u, n, p.ws_ml + u * S * G * 2, S);  // uniform branch
     } else {
-        for (int s = lane_id(); s < S; s += 64) m = p.ws_amin[u * S + s] < m ? p.ws_amin[u * S + s] : m;
-        m = wave_min_u64(m);
+        for (int s = lane_id(); s < S; s += 64) lowest = p.ws_amin[u * S + s] < lowest ? p.ws_amin[u * S + s] : lowest;
+        lowest = wave_min_u64(lowest);
     }
-    const int j = evict ? (int)~(uint32_t)m : -1;
+    const int j = evict ? (int)~(uint32_t)lowest : -1;
     const uint4 xj = load_stream(vb, row_off(j >= 0 ? j : 0, ss32, ce));  // used after the outputs
     // outputs: the splits in batches of kMergeBatch whose loads all go out
     // together (a split past S reads split s0 again and weighs 0), each batch
